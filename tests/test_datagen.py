@@ -1,0 +1,68 @@
+"""The seeded generator makes what its recipe says (sizes, moments, skew) and is a
+pure function of (seed, counter)."""
+import math
+
+import numpy as np
+import pytest
+
+
+def test_tiny_workload(gen):
+    w = gen.workload("tiny")
+    tr, te = gen.make(w)
+    assert len(tr) == 49_500 and len(te) == 500
+    cells = np.concatenate([tr["u"].astype(np.int64) * w["n"] + tr["v"], te["u"].astype(np.int64) * w["n"] + te["v"]])
+    assert len(np.unique(cells)) == 50_000  # distinct cells
+    assert tr["u"].min() >= 0 and tr["u"].max() < w["m"] and tr["v"].max() < w["n"]
+    r = tr["r"].astype(np.float64)
+    # r = p*.q* + N(0, 0.1): mean 0, variance 1 + 0.1
+    assert abs(r.mean()) < 0.03 and r.var() == pytest.approx(1.1, rel=0.03)
+    tr2, te2 = gen.make(w)
+    assert np.array_equal(tr, tr2) and np.array_equal(te, te2)
+
+
+def test_planted_factor_moments(gen):
+    w = gen.workload("netflix", m=20000, n=3000)
+    Ps, Qs = gen.planted(w)
+    var = 1 / math.sqrt(128)
+    assert float(Ps.var()) == pytest.approx(var, rel=0.01) and abs(float(Ps.mean())) < 2e-3
+    assert float(Qs.var()) == pytest.approx(var, rel=0.01)
+
+
+def test_netflix_shaped_ratings_and_skew(gen):
+    w = gen.workload("netflix", ntrain=1_000_000, ntest=1000)
+    tr, te = gen.make(w)
+    r = tr["r"]
+    assert set(np.unique(r).tolist()) <= {1.0, 2.0, 3.0, 4.0, 5.0}
+    assert 3.3 < float(r.mean()) < 3.8
+    # Zipf(1.0): the most popular rank has probability 1/H_N
+    for col, N in (("u", w["m"]), ("v", w["n"])):
+        H = float(np.sum(1.0 / np.arange(1, N + 1)))
+        top = np.bincount(tr[col], minlength=N).max() / len(tr)
+        assert top == pytest.approx(1.0 / H, rel=0.03)
+
+
+def test_zipf_slope(gen):
+    cdf, perm = gen.zipf_table(5000, 0.8, 123, 0)
+    pmf = np.diff(np.concatenate([[0.0], cdf]))
+    ranks = np.arange(1, 5001)
+    slope = np.polyfit(np.log(ranks), np.log(pmf), 1)[0]
+    assert slope == pytest.approx(-0.8, abs=1e-6)
+    assert sorted(perm.tolist()) == list(range(5000))
+
+
+def test_counter_draws_are_chunk_invariant(gen):
+    w = gen.workload("yahoo", m=5000, n=4000, ntrain=10000, ntest=0)
+    a = gen.draw(w, 0, 10000)
+    b = np.concatenate([gen.draw(w, 0, 3000), gen.draw(w, 3000, 7000)])
+    assert np.array_equal(a, b)
+    assert a["r"].min() >= 0 and a["r"].max() <= 5.0
+    assert np.allclose(a["r"] * 20, np.round(a["r"] * 20))
+
+
+def test_hugewiki_shape_items_uniform(gen):
+    w = gen.workload("hugewiki", m=200_000, ntrain=400_000, ntest=0)
+    a = gen.draw(w, 0, 400_000)
+    cv = np.bincount(a["v"], minlength=w["n"])
+    # uniform items: counts ~ Poisson(10)
+    assert cv.mean() == pytest.approx(400_000 / w["n"]) and cv.max() < 40
+    assert abs(float(a["r"].mean())) < 0.02 and float(a["r"].var()) == pytest.approx(2.0, rel=0.03)

@@ -1,0 +1,361 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+hand-worked examples, published test vectors, closed forms, invariants,
+library routines for special cases and brute force on tiny inputs."""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def samples(rows, orc):
+    a = np.zeros(len(rows), dtype=orc.SAMPLE_DTYPE)
+    for i, (u, v, r) in enumerate(rows):
+        a[i] = (u, v, r)
+    return a
+
+
+# ---------------------------------------------------------------------------- single update
+def test_k1_worked_example(orc):
+    g = gold("k1_update.json")
+    p, q = orc.sgd_step([g["p"]], [g["q"]], g["r"], g["lr"], g["lambda_p"], g["lambda_q"])
+    assert p[0] == g["p_new"] and q[0] == g["q_new"]
+    assert q[0] != g["q_new_if_q_used_updated_p"]
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_k1_worked_example_in_storage(orc, dtype):
+    """The same update applied through an epoch over one sample, for each storage type
+    (all values are exact in binary16)."""
+    g = gold("k1_update.json")
+    P = np.array([[g["p"]]], dtype=dtype)
+    Q = np.array([[g["q"]]], dtype=dtype)
+    orc.epoch_serial(P, Q, samples([(0, 0, g["r"])], orc), g["lr"], g["lambda_p"], g["lambda_q"])
+    assert float(P[0, 0]) == g["p_new"] and float(Q[0, 0]) == g["q_new"]
+
+
+def test_k2_worked_example(orc):
+    g = gold("k2_update.json")
+    p, q = orc.sgd_step(g["p"], g["q"], g["r"], g["lr"], g["lambda_p"], g["lambda_q"])
+    assert list(p) == g["p_new"] and list(q) == g["q_new"]
+
+
+def test_update_is_half_gradient_step(orc):
+    """(p' - p)/lr equals minus half the gradient of the per-sample cost
+    (r - p.q)^2 + lp |p|^2 + lq |q|^2, measured by central differences."""
+    rng = np.random.default_rng(7)
+    k = 6
+    p0, q0 = rng.normal(size=k), rng.normal(size=k)
+    r, lr, lp, lq = 1.7, 1e-3, 0.3, 0.11
+
+    def cost(p, q):
+        return (r - p @ q) ** 2 + lp * (p @ p) + lq * (q @ q)
+
+    p1, q1 = orc.sgd_step(p0, q0, r, lr, lp, lq)
+    h = 1e-6
+    for j in range(k):
+        e = np.zeros(k)
+        e[j] = h
+        gp = (cost(p0 + e, q0) - cost(p0 - e, q0)) / (2 * h)
+        gq = (cost(p0, q0 + e) - cost(p0, q0 - e)) / (2 * h)
+        assert (p1[j] - p0[j]) / lr == pytest.approx(-0.5 * gp, rel=1e-7, abs=1e-8)
+        assert (q1[j] - q0[j]) / lr == pytest.approx(-0.5 * gq, rel=1e-7, abs=1e-8)
+
+
+def test_transpose_symmetry(orc):
+    """Swapping the roles of users and items (u<->v, P<->Q, lp<->lq) gives the
+    mirrored result bit for bit: both vectors are updated from their old values."""
+    rng = np.random.default_rng(3)
+    m, n, k = 7, 5, 8
+    P = rng.uniform(0, 0.4, (m, k)).astype(np.float32)
+    Q = rng.uniform(0, 0.4, (n, k)).astype(np.float32)
+    S = samples([(rng.integers(m), rng.integers(n), rng.normal() + 1) for _ in range(60)], orc)
+    St = S.copy()
+    St["u"], St["v"] = S["v"], S["u"]
+    P1, Q1 = P.copy(), Q.copy()
+    orc.epoch_serial(P1, Q1, S, 0.05, 0.02, 0.07)
+    P2, Q2 = Q.copy(), P.copy()
+    orc.epoch_serial(P2, Q2, St, 0.05, 0.07, 0.02)
+    assert np.array_equal(P1, Q2) and np.array_equal(Q1, P2)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_lr_zero_is_identity(orc, dtype):
+    rng = np.random.default_rng(1)
+    m, n, k = 20, 15, 16
+    P, Q = orc.init_factors(m, n, k, 99, dtype)
+    S = samples([(rng.integers(m), rng.integers(n), rng.normal()) for _ in range(300)], orc)
+    P1, Q1 = P.copy(), Q.copy()
+    orc.epoch_serial(P1, Q1, S, 0.0, 0.05, 0.05)
+    assert np.array_equal(P1, P) and np.array_equal(Q1, Q)
+    P2, Q2 = P.copy(), Q.copy()
+    orc.epoch_wavefront(P2, Q2, S, 0.0, 0.05, 0.05, 4, 99, 0)
+    assert np.array_equal(P2, P) and np.array_equal(Q2, Q)
+
+
+def test_zero_error_no_regularisation_is_identity(orc):
+    P = np.array([[0.5, 0.25]], dtype=np.float32)
+    Q = np.array([[2.0, 4.0]], dtype=np.float32)
+    orc.epoch_serial(P, Q, samples([(0, 0, 2.0)], orc), 0.3, 0.0, 0.0)  # p.q = 2 exactly
+    assert P.tolist() == [[0.5, 0.25]] and Q.tolist() == [[2.0, 4.0]]
+
+
+def test_repeated_sample_fits_rating(orc):
+    P = np.array([[0.1, 0.2, 0.3]], dtype=np.float64).astype(np.float32)
+    Q = np.array([[0.3, 0.1, 0.2]], dtype=np.float32)
+    S = samples([(0, 0, 2.5)] * 2000, orc)
+    orc.epoch_serial(P, Q, S, 0.05, 0.0, 0.0)
+    assert float(P[0].astype(np.float64) @ Q[0].astype(np.float64)) == pytest.approx(2.5, abs=1e-5)
+
+
+def test_zero_padding_invariant(orc):
+    """Padding k=100 with 28 zero columns: the first 100 columns evolve bit for bit
+    as at k=100 and the padding stays exactly zero."""
+    rng = np.random.default_rng(5)
+    m, n = 30, 20
+    P = rng.uniform(0, 0.1, (m, 100)).astype(np.float32)
+    Q = rng.uniform(0, 0.1, (n, 100)).astype(np.float32)
+    S = samples([(rng.integers(m), rng.integers(n), rng.uniform(1, 5)) for _ in range(500)], orc)
+    Pp = np.zeros((m, 128), np.float32)
+    Qp = np.zeros((n, 128), np.float32)
+    Pp[:, :100], Qp[:, :100] = P, Q
+    orc.epoch_serial(P, Q, S, 0.01, 0.05, 0.05)
+    orc.epoch_serial(Pp, Qp, S, 0.01, 0.05, 0.05)
+    assert np.array_equal(Pp[:, :100], P) and np.array_equal(Qp[:, :100], Q)
+    assert not Pp[:, 100:].any() and not Qp[:, 100:].any()
+
+
+def test_planted_noiseless_training_rmse_goes_to_zero(orc):
+    """On an exactly rank-k rating matrix (every cell observed), serial SGD with
+    no regularisation drives the training RMSE towards 0."""
+    rng = np.random.default_rng(11)
+    m, n, k = 40, 30, 3
+    Ps, Qs = rng.normal(0, 0.7, (m, k)), rng.normal(0, 0.7, (n, k))
+    cells = [(u, v) for u in range(m) for v in range(n)]
+    rng.shuffle(cells)
+    S = samples([(u, v, float(Ps[u] @ Qs[v])) for u, v in cells], orc)
+    P = rng.uniform(0, 0.5, (m, k)).astype(np.float32)
+    Q = rng.uniform(0, 0.5, (n, k)).astype(np.float32)
+    hist = [orc.rmse(P, Q, S)]
+    for _ in range(300):
+        orc.epoch_serial(P, Q, S, 0.05, 0.0, 0.0)
+        hist.append(orc.rmse(P, Q, S))
+    assert hist[-1] < 0.01 * hist[0] and hist[-1] < 5e-3
+    assert hist[5] < hist[0] and hist[-1] <= hist[5]
+
+
+# ---------------------------------------------------------------------------- RMSE
+def test_rmse_hand_example(orc):
+    g = gold("rmse_hand.json")
+    P = np.array(g["P"], np.float32)
+    Q = np.array(g["Qt"], np.float32)
+    S = samples(g["samples"], orc)
+    assert orc.sq_errors(P, Q, S).tolist() == g["sq_errors"]
+    assert orc.rmse(P, Q, S) == math.sqrt(g["rmse_squared"])
+
+
+def test_rmse_special_cases(orc):
+    rng = np.random.default_rng(2)
+    S = samples([(rng.integers(5), rng.integers(4), rng.normal()) for _ in range(50)], orc)
+    P0 = np.zeros((5, 8), np.float32)
+    Q = rng.uniform(size=(4, 8)).astype(np.float32)
+    # P = 0: every prediction is 0, so RMSE = sqrt(mean r^2)
+    r = S["r"].astype(np.float64)
+    assert orc.rmse(P0, Q, S) == pytest.approx(math.sqrt(float(np.mean(r * r))), rel=1e-15)
+    assert orc.rmse(P0, Q, S[:0]) == 0.0
+    # ratings that are exactly the predictions (dyadic values): RMSE 0
+    P = np.full((5, 8), 0.5, np.float32)
+    Q = np.full((4, 8), 0.25, np.float32)
+    S2 = S.copy()
+    S2["r"] = 1.0
+    assert orc.rmse(P, Q, S2) == 0.0
+
+
+# ---------------------------------------------------------------------------- binary16
+def test_half_round_trip_exhaustive(orc):
+    for b in range(65536):
+        x = orc.half_to_double(b)
+        if math.isnan(x):
+            assert (b & 0x7c00) == 0x7c00 and (b & 0x3ff)
+            continue
+        assert orc.double_to_half(x) == b
+
+
+def test_half_ties_to_even(orc):
+    assert orc.double_to_half(1 + 2 ** -11) == 0x3C00  # tie between 1 and 1+2^-10 -> even (1)
+    assert orc.double_to_half(1 + 3 * 2 ** -11) == 0x3C02  # tie -> 1 + 2^-9 (even)
+    assert orc.double_to_half(65504.0) == 0x7BFF
+    assert orc.double_to_half(65519.99) == 0x7BFF
+    assert orc.double_to_half(65520.0) == 0x7C00
+    assert orc.double_to_half(2 ** -25) == 0x0000  # tie between 0 and the smallest subnormal
+    assert orc.double_to_half(3 * 2 ** -25) == 0x0002
+    assert orc.double_to_half(-0.0) == 0x8000
+
+
+def test_half_matches_numpy_conversion(orc):
+    """numpy converts binary64 to binary16 with a single round-to-nearest-even."""
+    rng = np.random.default_rng(0)
+    xs = np.concatenate([rng.normal(0, 1, 20000), rng.normal(0, 1e-5, 5000), rng.normal(0, 3e4, 5000),
+                         rng.uniform(0, 0.2, 20000)])
+    with np.errstate(over="ignore"):
+        ref = xs.astype(np.float16).view(np.uint16)
+    got = np.array([orc.double_to_half(float(x)) for x in xs], dtype=np.uint16)
+    assert np.array_equal(got, ref)
+
+
+# ---------------------------------------------------------------------------- SplitMix64 / init
+def test_splitmix64_published_vectors(orc):
+    for vec in gold("splitmix64.json")["vectors"]:
+        for i, o in enumerate(vec["outputs"]):
+            assert orc.splitmix64(vec["seed"], i) == int(o, 0)
+
+
+@pytest.mark.parametrize("k", [1, 32, 100, 128])
+def test_init_range_and_moments(orc, k):
+    P, Q = orc.init_factors(2000, 300, k, 12345, np.float32)
+    hi = 1.0 / math.sqrt(k)
+    for A in (P, Q):
+        assert A.min() >= 0.0 and A.max() < hi
+        assert float(A.mean()) == pytest.approx(0.5 * hi, rel=0.02)
+        assert float(A.var()) == pytest.approx(hi * hi / 12, rel=0.05)
+    assert not np.array_equal(P[:300], Q)  # distinct streams
+
+
+def test_init_deterministic_and_half_consistent(orc):
+    P1, Q1 = orc.init_factors(50, 40, 16, 7, np.float32)
+    P2, Q2 = orc.init_factors(50, 40, 16, 7, np.float32)
+    P3, _ = orc.init_factors(50, 40, 16, 8, np.float32)
+    assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2) and not np.array_equal(P1, P3)
+    Ph, Qh = orc.init_factors(50, 40, 16, 7, np.float16)
+    # binary16 init is the binary64 value rounded once; it lies within half a binary16 ulp
+    # of the binary32 rounding of the same value
+    ulp = np.spacing(Ph.astype(np.float16)).astype(np.float64)
+    assert np.all(np.abs(Ph.astype(np.float64) - P1.astype(np.float64)) <= 0.5 * ulp + 1e-9)
+
+
+# ---------------------------------------------------------------------------- schedules
+def test_fisher_yates_is_uniform(orc):
+    """All 3! orders appear with equal frequency over many streams (a Sattolo-style
+    off-by-one would produce only the 2 cyclic permutations)."""
+    counts = {}
+    N = 60000
+    for st in range(N):
+        key = tuple(orc.fisher_yates(orc.splitmix64(424242, st), 3))
+        counts[key] = counts.get(key, 0) + 1
+    assert len(counts) == 6
+    for c in counts.values():
+        assert abs(c - N / 6) < 5 * math.sqrt(N / 6)
+
+
+@pytest.mark.parametrize("s", [1, 2, 5, 32, 64])
+def test_sigma_is_latin_square(orc, s):
+    for t in range(3):
+        sig = orc.wavefront_sigma(2024, t, s)
+        for i in range(s):
+            assert sorted(sig[i]) == list(range(s))  # each worker visits every column once
+            assert sorted(sig[:, i]) == list(range(s))  # in each wave, workers use distinct columns
+    if s > 2:
+        assert not np.array_equal(orc.wavefront_sigma(2024, 0, s), orc.wavefront_sigma(2024, 1, s))
+
+
+def test_block_mapping(orc):
+    m, n, s = 480189, 17770, 32
+    assert orc.row_block(0, m, s) == 0 and orc.row_block(m - 1, m, s) == s - 1
+    assert orc.col_block(0, n, s) == 0 and orc.col_block(n - 1, n, s) == s - 1
+    # sizes of row blocks differ by at most one
+    rows = np.bincount([orc.row_block(u, 1000, 7) for u in range(1000)])
+    assert rows.max() - rows.min() <= 1 and rows.sum() == 1000
+
+
+def test_block_order_is_stable_bucketing(orc):
+    rng = np.random.default_rng(4)
+    m, n, s = 53, 41, 4
+    S = samples([(rng.integers(m), rng.integers(n), float(i)) for i in range(700)], orc)
+    order, start = orc.block_order(S, m, n, s)
+    assert sorted(order.tolist()) == list(range(700))
+    for b in range(s * s):
+        idx = order[start[b]:start[b + 1]]
+        assert np.all(np.diff(idx) > 0)  # array order kept inside a block
+        for i in idx:
+            assert orc.row_block(S[i]["u"], m, s) * s + orc.col_block(S[i]["v"], n, s) == b
+
+
+def _wavefront_sequence(orc, S, m, n, s, seed, t, reverse_workers=False):
+    order, start = orc.block_order(S, m, n, s)
+    sig = orc.wavefront_sigma(seed, t, s)
+    seq = []
+    for w in range(s):
+        workers = range(s - 1, -1, -1) if reverse_workers else range(s)
+        for i in workers:
+            b = i * s + sig[i, w]
+            seq.extend(order[start[b]:start[b + 1]].tolist())
+    return np.array(seq, dtype=np.int64)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_wavefront_blocks_commute(orc, dtype):
+    """Blocks of one wave share no row and no column (independent samples,
+    section 2.3), so the wavefront epoch equals a serial epoch over its schedule
+    with the workers of every wave taken in either order."""
+    rng = np.random.default_rng(9)
+    m, n, k, s, seed = 64, 48, 8, 4, 77
+    S = samples([(rng.integers(m), rng.integers(n), rng.uniform(1, 5)) for _ in range(3000)], orc)
+    P, Q = orc.init_factors(m, n, k, seed, dtype)
+    Pw, Qw = P.copy(), Q.copy()
+    orc.epoch_wavefront(Pw, Qw, S, 0.02, 0.05, 0.05, s, seed, 3)
+    for rev in (False, True):
+        seq = _wavefront_sequence(orc, S, m, n, s, seed, 3, rev)
+        assert sorted(seq.tolist()) == list(range(len(S)))
+        Ps, Qs = P.copy(), Q.copy()
+        orc.epoch_serial(Ps, Qs, S[seq], 0.02, 0.05, 0.05)
+        assert np.array_equal(Ps, Pw) and np.array_equal(Qs, Qw)
+
+
+def test_wavefront_single_block_is_serial(orc):
+    rng = np.random.default_rng(12)
+    S = samples([(rng.integers(20), rng.integers(10), rng.normal()) for _ in range(400)], orc)
+    P, Q = orc.init_factors(20, 10, 4, 5, np.float32)
+    P1, Q1, P2, Q2 = P.copy(), Q.copy(), P.copy(), Q.copy()
+    orc.epoch_wavefront(P1, Q1, S, 0.05, 0.01, 0.02, 1, 5, 0)
+    orc.epoch_serial(P2, Q2, S, 0.05, 0.01, 0.02)
+    assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2)
+
+
+def test_two_by_two_blocking_feasible_orders(orc):
+    """Brute force over the 24 orders of a 2 x 2 grid run by 2 workers: an order is
+    feasible when each pair issued together is independent (no shared row or
+    column).  Exactly 8 are, and every wavefront schedule is one of them."""
+    g = gold("blocking_2x2.json")
+    blocks = [(0, 0), (0, 1), (1, 0), (1, 1)]
+
+    def indep(a, b):
+        return a[0] != b[0] and a[1] != b[1]
+
+    feasible = {o for o in itertools.permutations(blocks) if indep(o[0], o[1]) and indep(o[2], o[3])}
+    assert len(list(itertools.permutations(blocks))) == g["orders"]
+    assert len(feasible) == g["feasible"]
+    seen = set()
+    for t in range(40):
+        sig = orc.wavefront_sigma(31337, t, 2)
+        for w0 in (0, 1):  # the two workers of a wave may be issued in either order
+            for w1 in (0, 1):
+                o = ((w0, sig[w0, 0]), (1 - w0, sig[1 - w0, 0]), (w1, sig[w1, 1]), (1 - w1, sig[1 - w1, 1]))
+                assert o in feasible
+                seen.add(o)
+    assert seen == feasible
+
+
+def test_hogwild_single_worker_is_serial_order(orc):
+    own = orc.hogwild_batch_owner(1000, 256, 1)
+    assert own.tolist() == [0, 0, 0, 0]
+    own = orc.hogwild_batch_owner(1025, 256, 3)
+    assert own.tolist() == [0, 1, 2, 0, 1]
