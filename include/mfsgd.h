@@ -1,0 +1,194 @@
+/*
+ * mfsgd.h -- C ABI of the MI355X (gfx950) SGD matrix-factorisation library.
+ *
+ * The library trains R ~ P x Q from sparse ratings with stochastic gradient
+ * descent, the method of Xie, Tan, Fong, Liang, "CuMF_SGD: Fast and Scalable
+ * Matrix Factorization" (arXiv 1610.05838):
+ *   - the per-sample update of section 2.2 (prediction error, then the
+ *     regularised update of p_u and q_v, both from their values before the
+ *     step),
+ *   - the two single-GPU schedules of section 3.2: batch-Hogwild!
+ *     (section 3.2.2) and wavefront-update (section 3.2.3),
+ *   - the test RMSE used as the convergence measure (section 3.2.4).
+ *
+ * Conventions for every call:
+ *   - Every entry point returns an int status: MFSGD_OK (0) or a negative
+ *     MFSGD_E* code; mfsgd_last_error() then describes the failure.  No C++
+ *     exception crosses the ABI.
+ *   - All calls act on one process-wide context (one model on the current
+ *     HIP device).  The library is not thread-safe: calls must not overlap.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default (null)
+ *     stream.  Calls documented as asynchronous only enqueue work.
+ *   - Sample arrays are caller-owned device memory holding packed 12-byte
+ *     mfsgd_sample records; they must stay alive and unchanged until the
+ *     work enqueued on them has completed.
+ *   - P, Q, the wavefront plan, tickets and all scratch are library-owned
+ *     device memory, released by mfsgd_finalize() or by the next mfsgd_init().
+ *   - Feature storage: P is m rows of k values and Q is stored transposed,
+ *     n rows of k values (row v is the item vector q_v, the paper's column v
+ *     of the k x n matrix Q), so both rows are contiguous.  Rows are padded
+ *     internally to a supported width with zero columns; the padding stays
+ *     exactly zero and is invisible through get/set.
+ */
+#ifndef MFSGD_H
+#define MFSGD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* One observed rating r of user u for item v (0-based), 12 bytes, packed.
+ * Section 3.2.2 sizes a sample as two integers and one float. */
+typedef struct {
+    int32_t u;
+    int32_t v;
+    float r;
+} mfsgd_sample;
+
+enum {
+    MFSGD_OK = 0,
+    MFSGD_EINVAL = -1,   /* bad argument, option, size or index range       */
+    MFSGD_ENOMEM = -2,   /* device or pinned-host allocation failed         */
+    MFSGD_EHIP = -3,     /* a HIP runtime call failed (message has details) */
+    MFSGD_ESTATE = -4,   /* call not valid in the current state             */
+    MFSGD_ETIMEOUT = -5, /* a wavefront ticket wait hit the spin limit      */
+    MFSGD_ENUMERIC = -6  /* non-finite RMSE                                 */
+};
+
+/* Schedules (section 3.2). */
+enum {
+    /* batch-Hogwild! (section 3.2.2): the sample array is cut into batches
+     * of f consecutive samples; batch b goes to worker b mod W, which updates
+     * its batches in increasing order, each sample in array order; workers
+     * do not lock.  One worker is one 64-lane wavefront. */
+    MFSGD_BATCH_HOGWILD = 0,
+    /* wavefront-update (section 3.2.3) on the s x s grid of the last
+     * mfsgd_plan: worker i owns row block i and visits the column blocks in
+     * the order sigma_i(w) = C[(i + O[w]) mod s], C and O permutations drawn
+     * per epoch, so the blocks of one wave share no row and no column.  A
+     * 1-D array of column tickets orders the waves: worker i starts wave w
+     * once column sigma_i(w) has been released by wave w-1.  A worker is a
+     * team of `waves_per_block` wavefronts that run batch-Hogwild! inside
+     * the block. */
+    MFSGD_WAVEFRONT = 1,
+    /* the same schedule with one wavefront per worker and each block's
+     * samples in their array order: the result then equals the serial
+     * update in wave order up to floating-point rounding (deterministic). */
+    MFSGD_WAVEFRONT_DET = 2
+};
+
+enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
+
+/* Options (integer valued).  Keys:
+ *   "dtype"           feature storage: MFSGD_FP32 (default) or MFSGD_FP16
+ *                     (binary16 storage, binary32 arithmetic, round to
+ *                     nearest even on store; section 3.1 "Half-precision").
+ *                     Takes effect at the next mfsgd_init.
+ *   "batch_f"         batch size f of batch-Hogwild!, a positive multiple of
+ *                     64 (default 256, the paper's choice in section 3.2.2).
+ *   "workers"         batch-Hogwild! worker count W (wavefronts); 0 = as many
+ *                     as the GPU holds resident (default 0).
+ *   "depth"           samples each wavefront keeps in flight: 1, 2, 4 or 8
+ *                     (default 4).  A wavefront forwards its own pending
+ *                     updates, so depth never changes the serial semantics
+ *                     of one worker.
+ *   "waves_per_block" wavefronts per wavefront-update worker, 1..16
+ *                     (default 8).
+ *   "spin_limit"      polls of a column ticket before the wait gives up with
+ *                     MFSGD_ETIMEOUT (default 2^24, each poll sleeps briefly).
+ *   "debug"           bit 0: count visits of every sample (read with
+ *                     mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
+ *                     schedule (MFSGD_DBG_TRACE).  Takes effect at the next
+ *                     epoch; costs one extra atomic per sample.
+ * Returns MFSGD_EINVAL for an unknown key or an out-of-range value. */
+int mfsgd_set_option(const char* key, int64_t value);
+int mfsgd_get_option(const char* key, int64_t* value);
+
+/* Allocate P (m x k) and Q (n x k) in the storage dtype on the current
+ * device and initialise every entry uniformly on [0, 1/sqrt(k)): entry j of
+ * row u of P is output u*k+j of the SplitMix64 stream keyed (seed, 1) -- the
+ * stream's state is output 1 of a SplitMix64 generator seeded with `seed` --
+ * whose top 24 bits times 2^-24 are multiplied in binary64 by 1/sqrt(k) and
+ * rounded once to the storage type; Q likewise with stream (seed, 2).  The
+ * paper fixes no initialisation; this one is reproducible bit for bit.
+ * Resets the epoch counter to 0 and drops any plan.  Synchronous.
+ * EINVAL: m or n not in [1, 2^31-1], k not in [1, 512]. */
+int mfsgd_init(int64_t m, int64_t n, int32_t k, uint64_t seed);
+
+/* Wavefront-update preparation (section 3.2.3): check every sample's indices
+ * (0 <= u < m, 0 <= v < n), cut the grid into s x s blocks (row block
+ * floor(u*s/m), column block floor(v*s/n)) and keep a library-owned copy of
+ * the samples grouped by block, in array order inside each block.  The plan
+ * is tied to (samples, nnz): a wavefront epoch on other samples returns
+ * MFSGD_ESTATE.  Synchronises `stream`.
+ * EINVAL: s not in [1, 64], nnz < 0, NULL samples with nnz > 0, or an
+ * out-of-range index (nothing is planned then). */
+int mfsgd_plan(const mfsgd_sample* samples, int64_t nnz, int32_t s, void* stream);
+
+/* One epoch: every one of the nnz samples is used for exactly one update
+ * (section 2.3), under `scheme`, with learning rate lr and regularisation
+ * lambda_p, lambda_q (section 2.2).  Asynchronous on `stream`; increments
+ * the epoch counter, which keys the wavefront column orders.  Indices are
+ * not checked here (use mfsgd_check_samples or mfsgd_plan): an index out of
+ * range is undefined behaviour.
+ * EINVAL: nnz < 0, NULL samples with nnz > 0, unknown scheme, non-finite lr
+ * or lambda.  ESTATE: no init, or a wavefront scheme without a plan for
+ * these samples. */
+int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
+                int32_t scheme, void* stream);
+
+/* Test RMSE (section 3.2.4): sqrt(sum over the ntest samples of
+ * (r - p_u . q_v)^2 / ntest), dot products in binary32, squares summed in
+ * binary64 in a fixed order (the result is reproducible bit for bit); 0 for
+ * ntest == 0.  Synchronises `stream` and writes *rmse_out.  Also reports a
+ * pending device error (ETIMEOUT) of earlier work on the stream.
+ * ENUMERIC: the result is not finite (it is still written). */
+int mfsgd_rmse(const mfsgd_sample* test, int64_t ntest, double* rmse_out, void* stream);
+
+/* Check that every sample index is in range.  Synchronises `stream`.
+ * EINVAL if any is not. */
+int mfsgd_check_samples(const mfsgd_sample* samples, int64_t nnz, void* stream);
+
+/* Wait for `stream` and report a device-side error of earlier epochs
+ * (MFSGD_ETIMEOUT if a ticket wait gave up; the flag is then cleared). */
+int mfsgd_sync(void* stream);
+
+/* Copy the factors out / in, compact m x k and n x k row-major in the
+ * storage dtype (4 or 2 bytes per value).  The pointers may be host or
+ * device memory.  Synchronise `stream`.  Either pointer may be NULL to skip
+ * that matrix. */
+int mfsgd_get_factors(void* P, void* Q, void* stream);
+int mfsgd_set_factors(const void* P, const void* Q, void* stream);
+
+/* Epoch counter (keys the per-epoch wavefront column orders); saved with the
+ * factors for checkpoint/resume. */
+int mfsgd_set_epoch(int64_t t);
+int64_t mfsgd_get_epoch(void);
+
+/* Debug buffers (see the "debug" option).  Synchronise `stream`.
+ *   MFSGD_DBG_VISITS : count = nnz of the last epoch, dst uint32[count] --
+ *                      how often each sample was used since the last epoch
+ *                      started (wavefront epochs count by position in the
+ *                      caller's array).
+ *   MFSGD_DBG_TRACE  : batch-Hogwild!: dst int32[ceil(nnz/f)], the worker
+ *                      that ran each batch; wavefront: dst int32[s*s],
+ *                      entry i*s+w = column block of worker i in wave w. */
+enum { MFSGD_DBG_VISITS = 1, MFSGD_DBG_TRACE = 2 };
+int mfsgd_debug_read(int32_t what, void* dst, int64_t count, void* stream);
+
+/* Release everything; the context returns to the un-initialised state. */
+int mfsgd_finalize(void);
+
+/* Text of the last failure in this thread ("" if none). */
+const char* mfsgd_last_error(void);
+
+/* Library version string. */
+const char* mfsgd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MFSGD_H */

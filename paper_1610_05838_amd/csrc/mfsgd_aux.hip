@@ -1,0 +1,253 @@
+// mfsgd_aux.hip -- storage-type independent kernels: RMSE final reduction,
+// index checks, ticket reset and the wavefront-update planner.
+#include "mfsgd_device.hpp"
+#include "mfsgd_launch.hpp"
+
+namespace mfsgd {
+
+// Pass 2 of the test RMSE: one workgroup adds the kRmseWaves partial sums in
+// a fixed order (strided per thread, then a fixed tree), so the result does
+// not depend on timing.
+__global__ __launch_bounds__(256) void k_rmse_final(const double* __restrict__ partial, int64_t ntest,
+                                                    double* __restrict__ out)
+{
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int i = threadIdx.x; i < kRmseWaves; i += 256)
+        acc += partial[i];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w)
+            red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        out[0] = ntest > 0 ? sqrt(red[0] / (double)ntest) : 0.0;
+}
+
+hipError_t rmse_final(const double* partial, int64_t ntest, double* out, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, st, partial, ntest, out);
+    return hipGetLastError();
+}
+
+__global__ void k_check(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n, int* bad)
+{
+    int found = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * blockDim.x) {
+        const int u = __builtin_nontemporal_load(&S[i].u);
+        const int v = __builtin_nontemporal_load(&S[i].v);
+        found |= (u < 0) | (u >= m) | (v < 0) | (v >= n);
+    }
+    if (found)
+        atomicOr(bad, 1);
+}
+
+hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int* bad, hipStream_t st)
+{
+    if (nnz <= 0)
+        return hipSuccess;
+    int64_t blocks = (nnz + 255) / 256;
+    if (blocks > 8192)
+        blocks = 8192;
+    hipLaunchKernelGGL(k_check, dim3((unsigned)blocks), dim3(256), 0, st, S, nnz, m, n, bad);
+    return hipGetLastError();
+}
+
+__global__ void k_reset_tickets(uint32_t* t, int s)
+{
+    if ((int)threadIdx.x < s)
+        t[threadIdx.x] = 0u;
+}
+
+hipError_t reset_tickets(uint32_t* t, int s, int* err, hipStream_t st)
+{
+    (void)err;
+    hipLaunchKernelGGL(k_reset_tickets, dim3(1), dim3(kMaxGrid), 0, st, t, s);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Planner: a stable counting sort of the samples by block id
+// (row block floor(u*s/m)) * s + (column block floor(v*s/n)).
+//   1. each of kPlanChunks wavefronts counts its contiguous chunk per block
+//      (and flags indices out of range);
+//   2. per block, an exclusive scan over the chunks;
+//   3. an exclusive scan over the blocks gives the block starts;
+//   4. each wavefront walks its chunk in order, 64 samples at a time, ranks
+//      equal blocks by lane (ballot peeling) and scatters the samples.
+// Chunks, steps and lanes are all taken in array order, so every block keeps
+// its samples in array order.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int block_of(int u, int v, int64_t m, int64_t n, int s)
+{
+    const int rb = (int)(((int64_t)u * s) / m);
+    const int cb = (int)(((int64_t)v * s) / n);
+    return rb * s + cb;
+}
+
+__global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
+                                                   int s, int32_t* __restrict__ counts, int* bad)
+{
+    __shared__ int hist[kMaxGrid * kMaxGrid];
+    const int nb = s * s;
+    for (int i = threadIdx.x; i < nb; i += 64)
+        hist[i] = 0;
+    __syncthreads();
+    const int64_t cs = (nnz + kPlanChunks - 1) / kPlanChunks;
+    const int64_t lo = (int64_t)blockIdx.x * cs;
+    const int64_t hi = lo + cs < nnz ? lo + cs : nnz;
+    int found = 0;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += 64) {
+        const int u = __builtin_nontemporal_load(&S[i].u);
+        const int v = __builtin_nontemporal_load(&S[i].v);
+        if (u < 0 || u >= m || v < 0 || v >= n) {
+            found = 1;
+            continue;
+        }
+        atomicAdd(&hist[block_of(u, v, m, n, s)], 1);
+    }
+    if (found)
+        atomicOr(bad, 1);
+    __syncthreads();
+    for (int b = threadIdx.x; b < nb; b += 64)
+        counts[(int64_t)b * kPlanChunks + blockIdx.x] = hist[b];
+}
+
+// exclusive scan of counts[b][0..kPlanChunks) in place, total to totals[b]
+__global__ __launch_bounds__(256) void k_plan_scan_chunks(int32_t* __restrict__ counts, int64_t* __restrict__ totals)
+{
+    constexpr int per = kPlanChunks / 256;
+    __shared__ int64_t part[256];
+    int32_t* row = counts + (int64_t)blockIdx.x * kPlanChunks;
+    int64_t local[per];
+    int64_t acc = 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        local[i] = row[threadIdx.x * per + i];
+        acc += local[i];
+    }
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    // inclusive Hillis-Steele scan of the 256 thread sums
+    for (int off = 1; off < 256; off <<= 1) {
+        int64_t add = (int)threadIdx.x >= off ? part[threadIdx.x - off] : 0;
+        __syncthreads();
+        part[threadIdx.x] += add;
+        __syncthreads();
+    }
+    int64_t run = threadIdx.x > 0 ? part[threadIdx.x - 1] : 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        row[threadIdx.x * per + i] = (int32_t)run;
+        run += local[i];
+    }
+    if (threadIdx.x == 255)
+        totals[blockIdx.x] = part[255];
+}
+
+// exclusive scan of the block totals: bstart[0..nb]
+__global__ __launch_bounds__(1024) void k_plan_scan_blocks(const int64_t* __restrict__ totals, int nb,
+                                                           int64_t* __restrict__ bstart)
+{
+    constexpr int per = (kMaxGrid * kMaxGrid) / 1024;
+    __shared__ int64_t part[1024];
+    int64_t local[per];
+    int64_t acc = 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        const int b = threadIdx.x * per + i;
+        local[i] = b < nb ? totals[b] : 0;
+        acc += local[i];
+    }
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        int64_t add = (int)threadIdx.x >= off ? part[threadIdx.x - off] : 0;
+        __syncthreads();
+        part[threadIdx.x] += add;
+        __syncthreads();
+    }
+    int64_t run = threadIdx.x > 0 ? part[threadIdx.x - 1] : 0;
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        const int b = threadIdx.x * per + i;
+        if (b < nb)
+            bstart[b] = run;
+        run += local[i];
+    }
+    if (threadIdx.x == 1023)
+        bstart[nb] = part[1023];
+}
+
+__global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
+                                                     int s, const int32_t* __restrict__ counts,
+                                                     const int64_t* __restrict__ bstart, Sample* __restrict__ Sp,
+                                                     int64_t* __restrict__ orig)
+{
+    __shared__ int64_t base[kMaxGrid * kMaxGrid];
+    const int nb = s * s;
+    for (int b = threadIdx.x; b < nb; b += 64)
+        base[b] = bstart[b] + counts[(int64_t)b * kPlanChunks + blockIdx.x];
+    __syncthreads();
+    const int lane = threadIdx.x;
+    const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+    const int64_t cs = (nnz + kPlanChunks - 1) / kPlanChunks;
+    const int64_t lo = (int64_t)blockIdx.x * cs;
+    const int64_t hi = lo + cs < nnz ? lo + cs : nnz;
+    for (int64_t c0 = lo; c0 < hi; c0 += 64) {
+        const int64_t i = c0 + lane;
+        bool valid = i < hi;
+        Sample x{0, 0, 0.f};
+        int b = -1;
+        if (valid) {
+            x.u = __builtin_nontemporal_load(&S[i].u);
+            x.v = __builtin_nontemporal_load(&S[i].v);
+            x.r = __builtin_nontemporal_load(&S[i].r);
+            valid = x.u >= 0 && x.u < m && x.v >= 0 && x.v < n; // the host never scatters a plan with bad indices
+            if (valid)
+                b = block_of(x.u, x.v, m, n, s);
+        }
+        uint64_t pending = __ballot(valid);
+        int64_t dest = -1;
+        while (pending) {
+            const int leader = __ffsll((unsigned long long)pending) - 1;
+            const int lb = __builtin_amdgcn_readlane(b, leader);
+            const uint64_t same = __ballot(b == lb) & pending;
+            const int64_t at = base[lb];
+            if ((same >> lane) & 1ull)
+                dest = at + __popcll(same & below);
+            __syncthreads();
+            if (lane == leader)
+                base[lb] = at + __popcll(same);
+            __syncthreads();
+            pending &= ~same;
+        }
+        if (valid) {
+            Sp[dest] = x;
+            if (orig)
+                orig[dest] = i;
+        }
+    }
+}
+
+hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
+                      hipStream_t st)
+{
+    const int nb = s * s;
+    hipLaunchKernelGGL(k_plan_count, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.counts, b.bad);
+    hipLaunchKernelGGL(k_plan_scan_chunks, dim3(nb), dim3(256), 0, st, b.counts, b.totals);
+    hipLaunchKernelGGL(k_plan_scan_blocks, dim3(1), dim3(1024), 0, st, b.totals, nb, b.bstart);
+    return hipGetLastError();
+}
+
+hipError_t plan_scatter(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
+                        hipStream_t st)
+{
+    hipLaunchKernelGGL(k_plan_scatter, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.counts, b.bstart, b.Sp,
+                       b.orig);
+    return hipGetLastError();
+}
+
+} // namespace mfsgd

@@ -1,0 +1,410 @@
+// mfsgd_device.hpp -- device building blocks of the gfx950 SGD-MF kernels.
+//
+// One SGD worker is one 64-lane wavefront.  A sample's feature rows (k values
+// each) are spread over the lanes, E = KP/64 consecutive values per lane (at
+// KP = 32 one value on each of the first 32 lanes), so every row is read and
+// written with one coalesced vector access per lane.  The dot product is
+// reduced across the wavefront with DPP row operations and the gfx950
+// permlane swaps (no LDS, no barrier), which leaves the same sum in every
+// lane.  Sample records are read 64 at a time (one per lane, streamed with
+// non-temporal loads) and broadcast with v_readlane, so the row addresses are
+// wave-uniform scalars.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mfsgd {
+
+struct Sample {
+    int32_t u;
+    int32_t v;
+    float r;
+};
+static_assert(sizeof(Sample) == 12, "a rating sample is two int32 and one float");
+
+typedef _Float16 half_t;
+
+template <typename T, int E>
+struct VecT;
+template <>
+struct VecT<float, 1> { typedef float type; };
+template <>
+struct VecT<float, 2> { typedef float type __attribute__((ext_vector_type(2))); };
+template <>
+struct VecT<float, 4> { typedef float type __attribute__((ext_vector_type(4))); };
+template <>
+struct VecT<float, 8> { typedef float type __attribute__((ext_vector_type(8))); };
+template <>
+struct VecT<half_t, 1> { typedef half_t type; };
+template <>
+struct VecT<half_t, 2> { typedef half_t type __attribute__((ext_vector_type(2))); };
+template <>
+struct VecT<half_t, 4> { typedef half_t type __attribute__((ext_vector_type(4))); };
+template <>
+struct VecT<half_t, 8> { typedef half_t type __attribute__((ext_vector_type(8))); };
+
+// Row geometry for a padded width KP.
+template <int KP>
+struct Geo {
+    static constexpr int E = KP >= 64 ? KP / 64 : 1; // values per lane
+    static constexpr int A = KP / E;                 // lanes that hold values (32 or 64)
+};
+
+template <typename T, int E>
+struct Row {
+    typedef typename VecT<T, E>::type V;
+    __device__ __forceinline__ static void load(const T* p, float (&x)[E])
+    {
+        V v = *reinterpret_cast<const V*>(p);
+        if constexpr (E == 1) {
+            x[0] = (float)v;
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                x[e] = (float)v[e];
+        }
+    }
+    __device__ __forceinline__ static void store(T* p, const float (&x)[E])
+    {
+        V v;
+        if constexpr (E == 1) {
+            v = (T)x[0]; // binary16: v_cvt_f16_f32, round to nearest even
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                v[e] = (T)x[e];
+        }
+        *reinterpret_cast<V*>(p) = v;
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Cross-lane sum over the 64 lanes; every lane receives the same value (each
+// step adds a pair of lanes in both orders, and IEEE addition commutes).
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float wave_sum(float x)
+{
+    x += dpp_mov<0xB1>(x);  // quad_perm [1,0,3,2]: pairs
+    x += dpp_mov<0x4E>(x);  // quad_perm [2,3,0,1]: quads
+    x += dpp_mov<0x141>(x); // row_half_mirror: 8 lanes
+    x += dpp_mov<0x140>(x); // row_mirror: 16 lanes
+    {
+        // v_permlane16_swap: odd rows of the first operand trade places with
+        // even rows of the second; with both operands x the two results hold,
+        // lane for lane, the sums of rows {0,1} and {2,3} split over both.
+        auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+    {
+        auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+    return x;
+}
+
+__device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ int64_t uniform64(int64_t x)
+{
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// ---------------------------------------------------------------------------
+// SplitMix64 (Steele, Lea, Flood 2014) in counter form: output number i of a
+// generator whose state starts at s0 is the finaliser applied to
+// s0 + (i+1) * golden-gamma.
+// ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ uint64_t sm64_at(uint64_t s0, uint64_t i)
+{
+    const uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+    uint64_t z = s0 + (i + 1ull) * kGamma;
+    z ^= z >> 30;
+    z *= 0xBF58476D1CE4E5B9ull;
+    z ^= z >> 27;
+    z *= 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    return z;
+}
+
+// Stream keys used by the library: stream `tag` is output `tag` of the
+// generator seeded with the user seed.
+enum : uint64_t { kTagP = 1, kTagQ = 2, kTagColPerm = 16, kTagWaveOffset = 17 };
+
+// Durstenfeld shuffle of 0..s-1: step i (from s-1 down to 1) swaps a[i]
+// with a[j], j = high 32 bits of draw (s-1-i) times (i+1), shifted down 32.
+__device__ __forceinline__ void shuffle_perm(uint64_t s0, int s, int* a)
+{
+    for (int i = 0; i < s; ++i)
+        a[i] = i;
+    for (int i = s - 1; i >= 1; --i) {
+        uint64_t x = sm64_at(s0, (uint64_t)(s - 1 - i));
+        int j = (int)(((x >> 32) * (uint64_t)(i + 1)) >> 32);
+        int t = a[i];
+        a[i] = a[j];
+        a[j] = t;
+    }
+}
+
+// Binary64 -> binary16 bits, round to nearest, ties to even, from the bit
+// patterns: keep the 11 significant bits that binary16 has at this exponent
+// (fewer below 2^-14) and round on the discarded remainder.
+__device__ __forceinline__ uint16_t f64_to_f16_bits(double x)
+{
+    uint64_t b = (uint64_t)__double_as_longlong(x);
+    uint16_t sgn = (uint16_t)((b >> 48) & 0x8000u);
+    int ef = (int)((b >> 52) & 0x7ff);
+    uint64_t frac = b & 0xFFFFFFFFFFFFFull;
+    if (ef == 0x7ff)
+        return (uint16_t)(sgn | (frac ? 0x7e00u : 0x7c00u));
+    if (ef == 0)
+        return sgn; // |x| < 2^-1022: far below the smallest binary16 subnormal
+    int e = ef - 1023;
+    if (e >= 16)
+        return (uint16_t)(sgn | 0x7c00u);
+    uint64_t sig = frac | (1ull << 52); // value = sig * 2^(e-52)
+    int qexp = (e < -14 ? -14 : e) - 10; // exponent of one binary16 unit here
+    int shift = qexp - (e - 52);         // >= 42
+    if (shift >= 54)
+        return sgn; // below half of the smallest subnormal
+    uint64_t n = sig >> shift;
+    uint64_t rem = sig & ((1ull << shift) - 1ull);
+    uint64_t halfway = 1ull << (shift - 1);
+    if (rem > halfway || (rem == halfway && (n & 1ull)))
+        ++n;
+    if (e < -14)
+        return (uint16_t)(sgn | (uint16_t)n); // n == 1024 is the smallest normal
+    if (n == 2048) {
+        n = 1024;
+        ++e;
+    }
+    if (e > 15)
+        return (uint16_t)(sgn | 0x7c00u);
+    return (uint16_t)(sgn | (uint16_t)((e + 15) << 10) | (uint16_t)(n - 1024));
+}
+
+template <typename T>
+__device__ __forceinline__ T from_f64(double x);
+template <>
+__device__ __forceinline__ float from_f64<float>(double x)
+{
+    return (float)x; // v_cvt_f32_f64: round to nearest even
+}
+template <>
+__device__ __forceinline__ half_t from_f64<half_t>(double x)
+{
+    uint16_t h = f64_to_f16_bits(x);
+    return __builtin_bit_cast(half_t, h);
+}
+
+// Debug hooks of one epoch.
+struct DebugSink {
+    uint32_t* visits;     // per caller-array sample, or nullptr
+    const int64_t* orig;  // planned position -> caller position, or nullptr
+    int32_t* trace;       // batch -> worker, or nullptr
+};
+
+// ---------------------------------------------------------------------------
+// One batch-Hogwild! worker (one wavefront).
+//
+// The worker's samples are the batches b = worker, worker+W, ... of f
+// consecutive samples of S[0..nnz), in increasing b, each in array order;
+// position q of this sequence is sample (worker + (q/f)*W)*f + q%f.  Rows of
+// the next D-1 samples are requested before the current sample is written
+// back; a requested row that an earlier, still-unwritten sample of this same
+// worker updates is replaced by that sample's new value (nearest wins), so
+// the worker's result is exactly the serial update of its sequence.
+// Updates of other workers race (Hogwild!).
+//
+// The loop body has no branch around a memory instruction (a look-ahead past
+// the end loads row 0 and is never used), so the compiler can keep all D
+// samples' loads in flight with counted waits.
+// ---------------------------------------------------------------------------
+template <int KP, typename T, int D>
+struct WorkerState {
+    static constexpr int E = Geo<KP>::E;
+    float sp[D][E], sq[D][E]; // rows in flight
+    int su[D], sv[D];
+    float sr[D];
+    float hp[D][E], hq[D][E]; // new rows of the last D samples
+    int hu[D], hv[D];
+};
+
+template <int KP, typename T, int D, bool DBG>
+__device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t worker,
+                                           int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
+                                           float lq, const DebugSink dbg)
+{
+    constexpr int E = Geo<KP>::E;
+    constexpr int A = Geo<KP>::A;
+    typedef Row<T, E> R;
+    static_assert(64 % D == 0 && D <= 32, "depth must divide 64");
+
+    const int lane = lane_id();
+    // lanes past the row width (KP = 32) mirror lane 0's address and never store
+    const int col = (A == 64 || lane < A) ? lane * E : 0;
+    const bool holds = (A == 64) || (lane < A);
+
+    int64_t c_batch = worker, n_batch = worker;
+    int c_off = 0, n_off = 0;
+    auto advance = [&](int64_t& b, int& o) {
+        o += 64;
+        if (o >= f) {
+            o = 0;
+            b += W;
+        }
+    };
+    auto load_chunk = [&](int64_t b, int o, int& cu, int& cv, float& cr, int& cnt) {
+        const int64_t s0 = b * (int64_t)f + o;
+        const int64_t rem = nnz - s0;
+        cnt = rem <= 0 ? 0 : (rem >= 64 ? 64 : (int)rem);
+        const int64_t i = s0 + (lane < cnt ? lane : 0);
+        const Sample* sp = S + (cnt > 0 ? i : 0);
+        cu = __builtin_nontemporal_load(&sp->u);
+        cv = __builtin_nontemporal_load(&sp->v);
+        cr = __builtin_nontemporal_load(&sp->r);
+    };
+
+    if (nnz <= 0 || worker * (int64_t)f >= nnz)
+        return;
+    int cU, cV, nU, nV, ccnt, ncnt;
+    float cR, nR;
+    load_chunk(c_batch, c_off, cU, cV, cR, ccnt);
+    advance(n_batch, n_off);
+    load_chunk(n_batch, n_off, nU, nV, nR, ncnt);
+
+    WorkerState<KP, T, D> st;
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        st.su[d] = st.sv[d] = st.hu[d] = st.hv[d] = -1;
+        st.sr[d] = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            st.sp[d][e] = st.sq[d][e] = st.hp[d][e] = st.hq[d][e] = 0.f;
+    }
+
+    // request the rows of the sample at lane `xl` of a chunk's metadata
+    auto issue = [&](int slot, int mu, int mv, float mr, int xl, int cnt) {
+        const bool ok = xl < cnt;
+        const int u = __builtin_amdgcn_readlane(mu, xl);
+        const int v = __builtin_amdgcn_readlane(mv, xl);
+        const float r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mr), xl));
+        st.su[slot] = ok ? u : -1;
+        st.sv[slot] = ok ? v : -1;
+        st.sr[slot] = r;
+        R::load(P + (int64_t)(ok ? u : 0) * KP + col, st.sp[slot]);
+        R::load(Q + (int64_t)(ok ? v : 0) * KP + col, st.sq[slot]);
+    };
+
+    // update the sample in slot j
+    auto process = [&](int j, int64_t pos) {
+        float p[E], q[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            p[e] = st.sp[j][e];
+            q[e] = st.sq[j][e];
+        }
+        const int u = st.su[j], v = st.sv[j];
+#pragma unroll
+        for (int d = D - 1; d >= 1; --d) {
+            const int h = (j - d + D) % D;
+            const bool fu = st.hu[h] == u, fv = st.hv[h] == v;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                p[e] = fu ? st.hp[h][e] : p[e];
+                q[e] = fv ? st.hq[h][e] : q[e];
+            }
+        }
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            dot += p[e] * q[e];
+        dot = wave_sum(dot);
+        const float err = st.sr[j] - dot;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const float pe = p[e], qe = q[e];
+            p[e] = pe + lr * (err * qe - lp * pe);
+            q[e] = qe + lr * (err * pe - lq * qe);
+        }
+        if (holds) {
+            R::store(P + (int64_t)u * KP + col, p);
+            R::store(Q + (int64_t)v * KP + col, q);
+        }
+        st.hu[j] = u;
+        st.hv[j] = v;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            st.hp[j][e] = p[e];
+            st.hq[j][e] = q[e];
+        }
+        if constexpr (DBG) {
+            if (dbg.visits && lane == 0) {
+                const int64_t idx = dbg.orig ? dbg.orig[pos] : pos;
+                atomicAdd(dbg.visits + idx, 1u);
+            }
+        }
+    };
+
+    // prologue: positions 0 .. D-2 of the first chunk
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d)
+        issue(d, cU, cV, cR, d, ccnt);
+
+    // One chunk of 64 positions; metadata of this chunk in (aU, aV, aR, acnt),
+    // of the next in (bU, bV, bR, bcnt).  The registers of a finished chunk
+    // receive the chunk after next, so the two sets alternate without copies.
+    auto chunk = [&](int& aU, int& aV, float& aR, int& acnt, int bU, int bV, float bR, int bcnt) -> bool {
+        const int64_t cbase = c_batch * (int64_t)f + c_off;
+        if constexpr (DBG) {
+            if (dbg.trace && c_off == 0 && lane == 0)
+                dbg.trace[c_batch] = (int32_t)worker;
+        }
+        for (int g = 0; g < 64 - D; g += D) { // look-ahead stays inside this chunk
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                const int x = g + j;
+                if (x >= acnt)
+                    return false;
+                issue((j + D - 1) % D, aU, aV, aR, x + D - 1, acnt);
+                process(j, cbase + x);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < D; ++j) { // last group: look-ahead reaches into the next chunk
+            const int x = 64 - D + j;
+            if (x >= acnt)
+                return false;
+            if (j == 0)
+                issue((j + D - 1) % D, aU, aV, aR, 63, acnt);
+            else
+                issue((j + D - 1) % D, bU, bV, bR, j - 1, bcnt);
+            process(j, cbase + x);
+        }
+        if (bcnt == 0)
+            return false;
+        c_batch = n_batch;
+        c_off = n_off;
+        advance(n_batch, n_off);
+        load_chunk(n_batch, n_off, aU, aV, aR, acnt);
+        return true;
+    };
+    for (;;) {
+        if (!chunk(cU, cV, cR, ccnt, nU, nV, nR, ncnt))
+            return;
+        if (!chunk(nU, nV, nR, ncnt, cU, cV, cR, ccnt))
+            return;
+    }
+}
+
+} // namespace mfsgd

@@ -1,0 +1,277 @@
+// mfsgd_kernels.hpp -- the gfx950 kernels and their launchers, instantiated
+// once per storage type (mfsgd_kernels_f32.hip, mfsgd_kernels_f16.hip).
+#pragma once
+
+#include "mfsgd_device.hpp"
+#include "mfsgd_launch.hpp"
+
+namespace mfsgd {
+
+constexpr int kHogwildBlock = 256; // 4 wavefronts per workgroup, each an independent worker
+
+// batch-Hogwild! epoch (section 3.2.2): wavefront w of the grid is worker w.
+template <int KP, typename T, int D, bool DBG>
+__global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restrict__ S, int64_t nnz, int64_t W,
+                                                           int f, T* __restrict__ P, T* __restrict__ Q, float lr,
+                                                           float lp, float lq, DebugSink dbg)
+{
+    const int64_t worker = uniform64((int64_t)blockIdx.x * (kHogwildBlock / 64) + (threadIdx.x >> 6));
+    if (worker >= W)
+        return;
+    run_worker<KP, T, D, DBG>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg);
+}
+
+// Wavefront-update epoch (section 3.2.3).  Workgroup i is worker i (a team of
+// blockDim/64 wavefronts) and owns row block i.  In wave w it takes column
+// block sigma_i(w) = C[(i + O[w]) mod s] once that column's ticket reads w,
+// runs batch-Hogwild! over the block with its wavefronts, and releases the
+// column by storing w+1.  Every column is used by exactly one worker per
+// wave, so the ticket of a column counts the waves completed on it.
+// Release/acquire at agent scope make one team's feature writes visible to
+// the next team that takes the column, whichever XCD either runs on.  A wait
+// that exceeds spin_limit polls raises *err and every team leaves.
+template <int KP, typename T, int D, bool DBG>
+__global__ __launch_bounds__(1024) void k_wavefront(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
+                                                    int s, uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
+                                                    T* __restrict__ Q, float lr, float lp, float lq, int f,
+                                                    uint32_t* tickets, uint32_t spin_limit, int* err, DebugSink dbg,
+                                                    int32_t* trace)
+{
+    __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
+    __shared__ int abort_all;
+    const int team = blockIdx.x;
+    const int waves = blockDim.x >> 6;
+    const int wv = uniform(threadIdx.x >> 6);
+    if (threadIdx.x == 0) {
+        shuffle_perm(sigma_c, s, Cperm);
+        shuffle_perm(sigma_o, s, Ooff);
+        abort_all = 0;
+    }
+    __syncthreads();
+    DebugSink inner = dbg;
+    inner.trace = nullptr;
+    for (int w = 0; w < s; ++w) {
+        const int col = Cperm[(team + Ooff[w]) % s];
+        if (threadIdx.x == 0) {
+            uint32_t polls = 0;
+            while (__hip_atomic_load(tickets + col, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != (uint32_t)w) {
+                if (++polls > spin_limit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                    __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    abort_all = 1;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(4);
+            }
+            if (trace)
+                trace[(int64_t)team * s + w] = col;
+        }
+        __syncthreads();
+        if (abort_all)
+            return;
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        const int64_t b = (int64_t)team * s + col;
+        const int64_t lo = bstart[b], hi = bstart[b + 1];
+        if (hi > lo) {
+            DebugSink blk = inner;
+            if (blk.orig)
+                blk.orig += lo;
+            run_worker<KP, T, D, DBG>(Sp + lo, hi - lo, waves, wv, f, P, Q, lr, lp, lq, blk);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __syncthreads();
+        if (threadIdx.x == 0)
+            __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Test RMSE, pass 1 (section 3.2.4): wavefront w of kRmseWaves sums the
+// squared errors of its contiguous share of the test samples in binary64.
+// Samples are independent here, so 8 are fetched before any is reduced.
+template <int KP, typename T>
+__global__ __launch_bounds__(256) void k_rmse_partial(const Sample* __restrict__ S, int64_t ntest,
+                                                      const T* __restrict__ P, const T* __restrict__ Q,
+                                                      double* __restrict__ partial)
+{
+    constexpr int E = Geo<KP>::E;
+    constexpr int A = Geo<KP>::A;
+    constexpr int U = 8;
+    typedef Row<T, E> R;
+    const int lane = lane_id();
+    const bool holds = (A == 64) || (lane < A);
+    const int col = lane * E;
+    const int64_t wave = uniform64((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6));
+    const int64_t share = (ntest + kRmseWaves - 1) / kRmseWaves;
+    const int64_t lo = wave * share;
+    const int64_t hi = lo + share < ntest ? lo + share : ntest;
+    double acc = 0.0;
+    for (int64_t c0 = lo; c0 < hi; c0 += 64) {
+        const int cnt = (int)(hi - c0 >= 64 ? 64 : hi - c0);
+        int cu = 0, cv = 0;
+        float cr = 0.f;
+        if (lane < cnt) {
+            cu = __builtin_nontemporal_load(&S[c0 + lane].u);
+            cv = __builtin_nontemporal_load(&S[c0 + lane].v);
+            cr = __builtin_nontemporal_load(&S[c0 + lane].r);
+        }
+        for (int i0 = 0; i0 < cnt; i0 += U) {
+            float p[U][E], q[U][E];
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int i = i0 + j;
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    p[j][e] = q[j][e] = 0.f;
+                if (i < cnt && holds) {
+                    const int u = __builtin_amdgcn_readlane(cu, i);
+                    const int v = __builtin_amdgcn_readlane(cv, i);
+                    R::load(P + (int64_t)u * KP + col, p[j]);
+                    R::load(Q + (int64_t)v * KP + col, q[j]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int i = i0 + j;
+                float dot = 0.f;
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    dot += p[j][e] * q[j][e];
+                dot = wave_sum(dot);
+                if (i < cnt) {
+                    const float r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cr), i));
+                    const double e = (double)(r - dot);
+                    acc += e * e;
+                }
+            }
+        }
+    }
+    if (lane == 0)
+        partial[wave] = acc;
+}
+
+template <int KP, typename T, int D, bool DBG>
+static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
+{
+    T* P = (T*)a.P;
+    T* Q = (T*)a.Q;
+    if (a.scheme == kSchemeHogwild) {
+        const int64_t blocks = (a.W + 3) / 4;
+        const DebugSink dbg{a.visits, nullptr, a.trace_batch};
+        hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st, a.S,
+                           a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg);
+    } else {
+        const DebugSink dbg{a.visits, a.orig, nullptr};
+        hipLaunchKernelGGL((k_wavefront<KP, T, D, DBG>), dim3((unsigned)a.s), dim3(64 * a.team_waves), 0, st, a.S,
+                           a.bstart, a.s, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets,
+                           a.spin_limit, a.err, dbg, a.trace_wave);
+    }
+    return hipGetLastError();
+}
+
+template <int KP, typename T, int D>
+static hipError_t launch_epoch_t(const EpochLaunch& a, hipStream_t st)
+{
+    if (a.visits || a.trace_batch)
+        return launch_epoch_d<KP, T, D, true>(a, st);
+    return launch_epoch_d<KP, T, D, false>(a, st);
+}
+
+template <int KP, typename T>
+static hipError_t launch_epoch_kp(const EpochLaunch& a, hipStream_t st)
+{
+    switch (a.depth) {
+    case 1: return launch_epoch_t<KP, T, 1>(a, st);
+    case 2: return launch_epoch_t<KP, T, 2>(a, st);
+    case 4: return launch_epoch_t<KP, T, 4>(a, st);
+    case 8: return launch_epoch_t<KP, T, 8>(a, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int KP, typename T, int D>
+static int occupancy_t()
+{
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild<KP, T, D, false>, kHogwildBlock, 0) != hipSuccess)
+        return 0;
+    return blocks * (kHogwildBlock / 64);
+}
+
+template <int KP, typename T>
+static int occupancy_kp(int depth)
+{
+    switch (depth) {
+    case 1: return occupancy_t<KP, T, 1>();
+    case 2: return occupancy_t<KP, T, 2>();
+    case 4: return occupancy_t<KP, T, 4>();
+    case 8: return occupancy_t<KP, T, 8>();
+    default: return 0;
+    }
+}
+
+template <typename T>
+__global__ void k_init(T* __restrict__ A, int64_t rows, int k, int KP, uint64_t stream, double inv_sqrt_k)
+{
+    const int64_t total = rows * KP;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / KP;
+        const int j = (int)(i - row * KP);
+        double val = 0.0;
+        if (j < k) {
+            const uint64_t x = sm64_at(stream, (uint64_t)(row * k + j));
+            val = (double)(x >> 40) * 0x1p-24 * inv_sqrt_k;
+        }
+        A[i] = from_f64<T>(val);
+    }
+}
+
+template <typename T>
+struct Dispatch {
+    static hipError_t epoch(const EpochLaunch& a, hipStream_t st)
+    {
+        switch (a.KP) {
+        case 32: return launch_epoch_kp<32, T>(a, st);
+        case 64: return launch_epoch_kp<64, T>(a, st);
+        case 128: return launch_epoch_kp<128, T>(a, st);
+        case 256: return launch_epoch_kp<256, T>(a, st);
+        case 512: return launch_epoch_kp<512, T>(a, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
+    static int occupancy(int KP, int depth)
+    {
+        switch (KP) {
+        case 32: return occupancy_kp<32, T>(depth);
+        case 64: return occupancy_kp<64, T>(depth);
+        case 128: return occupancy_kp<128, T>(depth);
+        case 256: return occupancy_kp<256, T>(depth);
+        case 512: return occupancy_kp<512, T>(depth);
+        default: return 0;
+        }
+    }
+    static hipError_t rmse(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
+                           hipStream_t st)
+    {
+        const dim3 grid(kRmseWaves / 4), block(256);
+        switch (KP) {
+        case 32: hipLaunchKernelGGL((k_rmse_partial<32, T>), grid, block, 0, st, S, ntest, (const T*)P, (const T*)Q, partial); break;
+        case 64: hipLaunchKernelGGL((k_rmse_partial<64, T>), grid, block, 0, st, S, ntest, (const T*)P, (const T*)Q, partial); break;
+        case 128: hipLaunchKernelGGL((k_rmse_partial<128, T>), grid, block, 0, st, S, ntest, (const T*)P, (const T*)Q, partial); break;
+        case 256: hipLaunchKernelGGL((k_rmse_partial<256, T>), grid, block, 0, st, S, ntest, (const T*)P, (const T*)Q, partial); break;
+        case 512: hipLaunchKernelGGL((k_rmse_partial<512, T>), grid, block, 0, st, S, ntest, (const T*)P, (const T*)Q, partial); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
+    static hipError_t init(void* A, int64_t rows, int k, int KP, uint64_t stream, double inv_sqrt_k, hipStream_t st)
+    {
+        const int64_t total = rows * KP;
+        int64_t blocks = (total + 255) / 256;
+        if (blocks > 65536)
+            blocks = 65536;
+        hipLaunchKernelGGL((k_init<T>), dim3((unsigned)blocks), dim3(256), 0, st, (T*)A, rows, k, KP, stream,
+                           inv_sqrt_k);
+        return hipGetLastError();
+    }
+};
+
+} // namespace mfsgd

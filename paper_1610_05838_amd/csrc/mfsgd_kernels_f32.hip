@@ -1,0 +1,21 @@
+// mfsgd_kernels_f32.hip -- kernel instantiations for binary32 feature storage.
+#include "mfsgd_kernels.hpp"
+
+namespace mfsgd {
+
+hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st) { return Dispatch<float>::epoch(a, st); }
+
+int occupancy_f32(int KP, int depth) { return Dispatch<float>::occupancy(KP, depth); }
+
+hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
+                           hipStream_t st)
+{
+    return Dispatch<float>::rmse(KP, S, ntest, P, Q, partial, st);
+}
+
+hipError_t init_f32(void* A, int64_t rows, int k, int KP, uint64_t stream, double inv_sqrt_k, hipStream_t st)
+{
+    return Dispatch<float>::init(A, rows, k, KP, stream, inv_sqrt_k, st);
+}
+
+} // namespace mfsgd

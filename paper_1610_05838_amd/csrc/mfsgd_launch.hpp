@@ -1,0 +1,78 @@
+// mfsgd_launch.hpp -- host-side launch interface between the C-ABI layer and
+// the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mfsgd {
+
+struct Sample;
+
+constexpr int kMaxGrid = 64;      // largest wavefront-update grid side s
+constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never changes
+constexpr int kSchemeHogwild = 0;
+constexpr int kSchemeWavefront = 1;
+
+struct DebugSink;
+
+struct EpochLaunch {
+    int scheme;  // kSchemeHogwild or kSchemeWavefront
+    int KP;      // padded row width
+    int depth;   // samples in flight per wavefront
+    const Sample* S;
+    int64_t nnz;
+    int64_t W;   // batch-Hogwild! workers
+    int f;       // batch size
+    void* P;
+    void* Q;
+    float lr, lp, lq;
+    // wavefront-update
+    const int64_t* bstart;
+    int s;
+    int team_waves;
+    uint64_t sigma_c, sigma_o;
+    uint32_t* tickets;
+    uint32_t spin_limit;
+    int* err;
+    int32_t* trace_wave;
+    // debug
+    uint32_t* visits;
+    const int64_t* orig;
+    int32_t* trace_batch;
+};
+
+// Implemented per storage type in mfsgd_kernels_f32.hip / mfsgd_kernels_f16.hip.
+hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st);
+hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st);
+int occupancy_f32(int KP, int depth);
+int occupancy_f16(int KP, int depth);
+hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
+                            hipStream_t st);
+hipError_t rmse_partial_f16(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
+                            hipStream_t st);
+hipError_t init_f32(void* A, int64_t rows, int k, int KP, uint64_t stream, double inv_sqrt_k, hipStream_t st);
+hipError_t init_f16(void* A, int64_t rows, int k, int KP, uint64_t stream, double inv_sqrt_k, hipStream_t st);
+
+// Implemented in mfsgd_aux.hip (type-independent kernels).
+hipError_t rmse_final(const double* partial, int64_t ntest, double* out, hipStream_t st);
+hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int* bad, hipStream_t st);
+hipError_t reset_tickets(uint32_t* t, int s, int* err, hipStream_t st);
+// stable bucketing of samples into the s x s grid
+struct PlanBuffers {
+    int32_t* counts;   // s*s*chunks, bin-major
+    int64_t* totals;   // s*s
+    int64_t* bstart;   // s*s+1
+    Sample* Sp;        // planned copy
+    int64_t* orig;     // planned position -> caller position (optional)
+    int* bad;          // index-range flag
+};
+constexpr int kPlanChunks = 2048;
+// counts, per-block scans and block starts; raises *b.bad on an index out of range
+hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
+                      hipStream_t st);
+// scatter into the planned copy (run only after plan_build reported no bad index)
+hipError_t plan_scatter(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
+                        hipStream_t st);
+
+} // namespace mfsgd

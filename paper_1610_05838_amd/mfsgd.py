@@ -1,0 +1,193 @@
+"""Thin ctypes binding of ``libmfsgd.so`` (C ABI in ``include/mfsgd.h``).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of the library.  Device arrays are torch tensors on the current GPU;
+streams are torch streams (default: ``torch.cuda.current_stream()``).
+
+Samples are int32 tensors of shape (nnz, 3) whose columns hold u, v and the
+bit pattern of the float32 rating r -- exactly the packed 12-byte records the
+library reads.  ``samples_to_device`` builds one from a numpy structured array.
+
+The library is loaded on first use.  If it has not been built the binding
+raises ``ImportError``: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch  # loads the HIP runtime that the library then shares (same SONAME)
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmfsgd.so")
+
+OK, EINVAL, ENOMEM, EHIP, ESTATE, ETIMEOUT, ENUMERIC = 0, -1, -2, -3, -4, -5, -6
+BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET = 0, 1, 2
+FP32, FP16 = 0, 1
+DBG_VISITS, DBG_TRACE = 1, 2
+
+SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET}
+
+SAMPLE_DTYPE = np.dtype([("u", "<i4"), ("v", "<i4"), ("r", "<f4")])
+
+
+class MfsgdError(RuntimeError):
+    def __init__(self, code: int, fn: str, msg: str):
+        super().__init__(f"{fn} failed with status {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                              "(hipcc for gfx950); there is no CPU fallback")
+        L = C.CDLL(LIB_PATH)
+        i32, i64, u64, f32, vp = C.c_int32, C.c_int64, C.c_uint64, C.c_float, C.c_void_p
+        sig = {
+            "mfsgd_set_option": ([C.c_char_p, i64], C.c_int),
+            "mfsgd_get_option": ([C.c_char_p, C.POINTER(i64)], C.c_int),
+            "mfsgd_init": ([i64, i64, i32, u64], C.c_int),
+            "mfsgd_plan": ([vp, i64, i32, vp], C.c_int),
+            "mfsgd_epoch": ([vp, i64, f32, f32, f32, i32, vp], C.c_int),
+            "mfsgd_rmse": ([vp, i64, C.POINTER(C.c_double), vp], C.c_int),
+            "mfsgd_check_samples": ([vp, i64, vp], C.c_int),
+            "mfsgd_sync": ([vp], C.c_int),
+            "mfsgd_get_factors": ([vp, vp, vp], C.c_int),
+            "mfsgd_set_factors": ([vp, vp, vp], C.c_int),
+            "mfsgd_set_epoch": ([i64], C.c_int),
+            "mfsgd_get_epoch": ([], i64),
+            "mfsgd_debug_read": ([i32, vp, i64, vp], C.c_int),
+            "mfsgd_finalize": ([], C.c_int),
+            "mfsgd_last_error": ([], C.c_char_p),
+            "mfsgd_version": ([], C.c_char_p),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, fn: str) -> int:
+    if rc != OK:
+        raise MfsgdError(rc, fn, lib().mfsgd_last_error().decode())
+    return rc
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _samples_ptr(t: torch.Tensor):
+    if t.dtype != torch.int32 or t.dim() != 2 or t.shape[1] != 3 or not t.is_contiguous() or not t.is_cuda:
+        raise TypeError("samples must be a contiguous int32 cuda tensor of shape (nnz, 3)")
+    return C.c_void_p(t.data_ptr() if t.numel() else 0), t.shape[0]
+
+
+def samples_to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
+    """numpy structured (u, v, r) records -> int32 (nnz, 3) device tensor."""
+    a = np.ascontiguousarray(a)
+    assert a.dtype == SAMPLE_DTYPE
+    t = torch.from_numpy(a.view(np.int32).reshape(-1, 3).copy())
+    return t.to(device)
+
+
+def version() -> str:
+    return lib().mfsgd_version().decode()
+
+
+def set_option(key: str, value: int) -> None:
+    _check(lib().mfsgd_set_option(key.encode(), int(value)), "mfsgd_set_option")
+
+
+def get_option(key: str) -> int:
+    v = C.c_int64()
+    _check(lib().mfsgd_get_option(key.encode(), C.byref(v)), "mfsgd_get_option")
+    return v.value
+
+
+def init(m: int, n: int, k: int, seed: int) -> None:
+    _check(lib().mfsgd_init(m, n, k, seed), "mfsgd_init")
+
+
+def plan(samples: torch.Tensor, s: int, stream=None) -> None:
+    p, nnz = _samples_ptr(samples)
+    _check(lib().mfsgd_plan(p, nnz, s, _stream(stream)), "mfsgd_plan")
+
+
+def epoch(samples: torch.Tensor, lr: float, lambda_p: float, lambda_q: float, scheme="hogwild",
+          stream=None) -> None:
+    p, nnz = _samples_ptr(samples)
+    sc = SCHEMES[scheme] if isinstance(scheme, str) else int(scheme)
+    _check(lib().mfsgd_epoch(p, nnz, lr, lambda_p, lambda_q, sc, _stream(stream)), "mfsgd_epoch")
+
+
+def rmse(test: torch.Tensor, stream=None) -> float:
+    p, n = _samples_ptr(test)
+    out = C.c_double()
+    _check(lib().mfsgd_rmse(p, n, C.byref(out), _stream(stream)), "mfsgd_rmse")
+    return out.value
+
+
+def check_samples(samples: torch.Tensor, stream=None) -> None:
+    p, nnz = _samples_ptr(samples)
+    _check(lib().mfsgd_check_samples(p, nnz, _stream(stream)), "mfsgd_check_samples")
+
+
+def sync(stream=None) -> None:
+    _check(lib().mfsgd_sync(_stream(stream)), "mfsgd_sync")
+
+
+def _storage_dtype():
+    return torch.float16 if get_option("dtype") == FP16 else torch.float32
+
+
+def get_factors(m: int, n: int, k: int, dtype=None, device="cuda", stream=None):
+    """(P, Q) copies, shapes (m, k) and (n, k), storage dtype of the model."""
+    dtype = dtype or _storage_dtype()
+    P = torch.empty((m, k), dtype=dtype, device=device)
+    Q = torch.empty((n, k), dtype=dtype, device=device)
+    _check(lib().mfsgd_get_factors(C.c_void_p(P.data_ptr()), C.c_void_p(Q.data_ptr()), _stream(stream)),
+           "mfsgd_get_factors")
+    return P, Q
+
+
+def set_factors(P: torch.Tensor, Q: torch.Tensor, stream=None) -> None:
+    P = P.contiguous()
+    Q = Q.contiguous()
+    _check(lib().mfsgd_set_factors(C.c_void_p(P.data_ptr()), C.c_void_p(Q.data_ptr()), _stream(stream)),
+           "mfsgd_set_factors")
+
+
+def set_epoch(t: int) -> None:
+    _check(lib().mfsgd_set_epoch(t), "mfsgd_set_epoch")
+
+
+def get_epoch() -> int:
+    return lib().mfsgd_get_epoch()
+
+
+def debug_visits(nnz: int, stream=None) -> torch.Tensor:
+    out = torch.empty(nnz, dtype=torch.int32, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_VISITS, C.c_void_p(out.data_ptr()), nnz, _stream(stream)), "mfsgd_debug_read")
+    return out
+
+
+def debug_trace(count: int, stream=None) -> torch.Tensor:
+    out = torch.empty(count, dtype=torch.int32, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_TRACE, C.c_void_p(out.data_ptr()), count, _stream(stream)),
+           "mfsgd_debug_read")
+    return out
+
+
+def finalize() -> None:
+    _check(lib().mfsgd_finalize(), "mfsgd_finalize")

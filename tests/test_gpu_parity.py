@@ -1,0 +1,354 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the same
+seeded inputs.
+
+Tolerances (max-abs over every factor entry after one deterministic epoch):
+binary32 storage 1e-4, binary16 storage 2e-2; test RMSE of the same factors
+relative 1e-6; Hogwild! test RMSE after N epochs within 1e-3 (binary32) /
+5e-3 (binary16) of the serial oracle's.  The GPU computes the update in
+binary32 with fused multiply-adds and a tree-ordered dot product, the oracle in
+binary64 with one rounding to storage per write, so results agree to rounding
+and not bit for bit; integer work (initialisation bits, schedules, visit
+counts) is compared exactly.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {np.float32: 1e-4, np.float16: 2e-2}
+DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=4, waves_per_block=8, spin_limit=1 << 24, debug=0)
+
+
+@pytest.fixture(scope="module")
+def M():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1610_05838_amd import mfsgd
+    mfsgd.lib()
+    yield mfsgd
+    mfsgd.finalize()
+
+
+def setup(M, m, n, k, seed, dtype=np.float32, **opts):
+    o = dict(DEFAULTS)
+    o["dtype"] = 1 if dtype == np.float16 else 0
+    o.update(opts)
+    for key, val in o.items():
+        M.set_option(key, val)
+    M.init(m, n, k, seed)
+
+
+def factors(M, m, n, k, dtype):
+    P, Q = M.get_factors(m, n, k)
+    return P.cpu().numpy().astype(dtype), Q.cpu().numpy().astype(dtype)
+
+
+def rand_samples(rng, m, n, nnz, lo=1.0, hi=5.0):
+    a = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    a["u"] = rng.integers(0, m, nnz)
+    a["v"] = rng.integers(0, n, nnz)
+    a["r"] = rng.uniform(lo, hi, nnz).astype(np.float32)
+    return a
+
+
+def maxabs(a, b):
+    return float(np.max(np.abs(a.astype(np.float64) - b.astype(np.float64)))) if a.size else 0.0
+
+
+# ---------------------------------------------------------------------------- initialisation
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [1, 32, 100, 128, 300])
+def test_init_bit_exact(M, dtype, k):
+    m, n, seed = 301, 203, 0xC0FFEE + k
+    setup(M, m, n, k, seed, dtype)
+    P, Q = factors(M, m, n, k, dtype)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    iv = np.uint32 if dtype == np.float32 else np.uint16
+    assert np.array_equal(P.view(iv), Po.view(iv)) and np.array_equal(Q.view(iv), Qo.view(iv))
+
+
+def test_set_get_round_trip(M):
+    import torch
+    setup(M, 40, 30, 100, 1)
+    rng = np.random.default_rng(0)
+    P = torch.tensor(rng.normal(size=(40, 100)), dtype=torch.float32, device="cuda")
+    Q = torch.tensor(rng.normal(size=(30, 100)), dtype=torch.float32, device="cuda")
+    M.set_factors(P, Q)
+    P2, Q2 = M.get_factors(40, 30, 100)
+    assert torch.equal(P, P2) and torch.equal(Q, Q2)
+
+
+# ---------------------------------------------------------------------------- RMSE
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [32, 128])
+def test_rmse_matches_oracle(M, dtype, k):
+    import torch
+    m, n = 5000, 700
+    setup(M, m, n, k, 5, dtype)
+    rng = np.random.default_rng(k)
+    P = rng.uniform(0, 0.3, (m, k)).astype(dtype)
+    Q = rng.uniform(0, 0.3, (n, k)).astype(dtype)
+    td = torch.float16 if dtype == np.float16 else torch.float32
+    M.set_factors(torch.from_numpy(P).to("cuda", td), torch.from_numpy(Q).to("cuda", td))
+    for ntest in (1, 63, 64, 65, 10_007, 300_001):
+        T = rand_samples(rng, m, n, ntest)
+        got = M.rmse(M.samples_to_device(T))
+        want = oracle.rmse(P, Q, T)
+        assert got == pytest.approx(want, rel=1e-6)
+        assert M.rmse(M.samples_to_device(T)) == got  # fixed reduction order
+    assert M.rmse(M.samples_to_device(T[:0])) == 0.0
+
+
+def test_rmse_hand_example(M):
+    import json
+    import os
+    import torch
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "rmse_hand.json")))
+    setup(M, 2, 2, 2, 0)
+    M.set_factors(torch.tensor(g["P"], device="cuda"), torch.tensor(g["Qt"], device="cuda"))
+    T = np.array([tuple(x) for x in g["samples"]], dtype=oracle.SAMPLE_DTYPE)
+    assert M.rmse(M.samples_to_device(T)) == math.sqrt(g["rmse_squared"])
+
+
+# ---------------------------------------------------------------------------- single worker = serial
+def forwarding_stress(rng, nnz):
+    """Tiny grid: consecutive samples share rows and columns all the time."""
+    return rand_samples(rng, 7, 5, nnz)
+
+
+@pytest.mark.parametrize("depth", [1, 2, 4, 8])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [32, 100, 128, 256])
+def test_single_worker_equals_serial(M, depth, dtype, k):
+    rng = np.random.default_rng(depth * 1000 + k)
+    for m, n, nnz in ((7, 5, 2000), (400, 300, 6001)):
+        S = rand_samples(rng, m, n, nnz) if m > 7 else forwarding_stress(rng, nnz)
+        seed = 77 + k
+        setup(M, m, n, k, seed, dtype, workers=1, depth=depth)
+        M.epoch(M.samples_to_device(S), 0.01, 0.05, 0.04, "hogwild")
+        P, Q = factors(M, m, n, k, dtype)
+        Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+        oracle.epoch_serial(Po, Qo, S, 0.01, 0.05, 0.04)
+        assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype], (m, n)
+
+
+def test_tiny_workload_single_worker_equals_serial(M, gen):
+    w = gen.workload("tiny")
+    S, T = gen.make(w)
+    setup(M, w["m"], w["n"], w["k"], w["seed"], workers=1)
+    dS = M.samples_to_device(S)
+    Po, Qo = oracle.init_factors(w["m"], w["n"], w["k"], w["seed"], np.float32)
+    for t in range(2):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+        oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
+    P, Q = factors(M, w["m"], w["n"], w["k"], np.float32)
+    assert maxabs(P, Po) <= 1e-4 and maxabs(Q, Qo) <= 1e-4
+    assert M.rmse(M.samples_to_device(T)) == pytest.approx(oracle.rmse(Po, Qo, T), abs=1e-5)
+
+
+# ---------------------------------------------------------------------------- schedules, coverage
+def test_hogwild_schedule_and_coverage(M):
+    rng = np.random.default_rng(3)
+    m, n, nnz = 3000, 2000, 1_000_003  # ragged last batch
+    S = rand_samples(rng, m, n, nnz)
+    setup(M, m, n, 128, 9, debug=3)
+    W = 1000
+    M.set_option("workers", W)
+    M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
+    vis = M.debug_visits(nnz).cpu().numpy()
+    assert np.all(vis == 1)
+    nb = (nnz + 255) // 256
+    tr = M.debug_trace(nb).cpu().numpy()
+    assert np.array_equal(tr, oracle.hogwild_batch_owner(nnz, 256, W))
+    # auto worker count: still every sample exactly once
+    M.set_option("workers", 0)
+    M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
+    assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+
+
+@pytest.mark.parametrize("scheme", ["wavefront", "wavefront_det"])
+def test_wavefront_schedule_and_coverage(M, scheme):
+    rng = np.random.default_rng(4)
+    m, n, nnz, s, seed = 2000, 1500, 200_001, 8, 1234
+    S = rand_samples(rng, m, n, nnz)
+    setup(M, m, n, 64, seed, debug=3)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    for t in range(3):
+        M.epoch(dS, 0.001, 0.05, 0.05, scheme)
+        assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+        tr = M.debug_trace(s * s).cpu().numpy().reshape(s, s)
+        assert np.array_equal(tr, oracle.wavefront_sigma(seed, t, s))
+
+
+# ---------------------------------------------------------------------------- deterministic wavefront
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("s", [1, 3, 8, 32])
+def test_wavefront_det_matches_oracle(M, gen, dtype, s):
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, dtype)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(2):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
+        oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, t)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+
+
+def test_wavefront_det_k128_zipf(M, gen):
+    w = gen.workload("netflix", m=20_000, n=3_000, ntrain=400_000, ntest=0)
+    S = gen.draw(w, 0, w["ntrain"])
+    m, n, k, seed, s = w["m"], w["n"], w["k"], w["seed"], 16
+    setup(M, m, n, k, seed)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
+    Po, Qo = oracle.init_factors(m, n, k, seed, np.float32)
+    oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0)
+    P, Q = factors(M, m, n, k, np.float32)
+    assert maxabs(P, Po) <= 1e-4 and maxabs(Q, Qo) <= 1e-4
+
+
+def test_checkpoint_resume_is_bitwise(M, gen):
+    import torch
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    m, n, k, seed, s = w["m"], w["n"], w["k"], w["seed"], 5
+    setup(M, m, n, k, seed)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    M.epoch(dS, 0.01, 0.05, 0.05, "wavefront_det")
+    M.epoch(dS, 0.01, 0.05, 0.05, "wavefront_det")
+    P2, Q2 = M.get_factors(m, n, k)
+    setup(M, m, n, k, seed)
+    M.plan(dS, s)
+    M.epoch(dS, 0.01, 0.05, 0.05, "wavefront_det")
+    P1, Q1 = M.get_factors(m, n, k)
+    t = M.get_epoch()
+    setup(M, m, n, k, 999)  # a different model, then restore
+    M.set_factors(P1, Q1)
+    M.set_epoch(t)
+    M.plan(dS, s)
+    M.epoch(dS, 0.01, 0.05, 0.05, "wavefront_det")
+    P3, Q3 = M.get_factors(m, n, k)
+    assert torch.equal(P2, P3) and torch.equal(Q2, Q3)
+
+
+# ---------------------------------------------------------------------------- invariants
+@pytest.mark.parametrize("scheme", ["hogwild", "wavefront", "wavefront_det"])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_lr_zero_is_identity(M, scheme, dtype):
+    import torch
+    rng = np.random.default_rng(8)
+    m, n, k = 900, 700, 128
+    S = rand_samples(rng, m, n, 300_000)
+    setup(M, m, n, k, 3, dtype)
+    dS = M.samples_to_device(S)
+    if scheme != "hogwild":
+        M.plan(dS, 8)
+    P0, Q0 = M.get_factors(m, n, k)
+    M.epoch(dS, 0.0, 0.05, 0.05, scheme)
+    P1, Q1 = M.get_factors(m, n, k)
+    assert torch.equal(P0, P1) and torch.equal(Q0, Q1)
+
+
+# ---------------------------------------------------------------------------- Hogwild! convergence parity
+@pytest.mark.parametrize("dtype,tol", [(np.float32, 1e-3), (np.float16, 5e-3)])
+def test_hogwild_rmse_gap_tiny(M, gen, dtype, tol):
+    w = gen.workload("tiny")
+    S, T = gen.make(w)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, dtype)
+    dS, dT = M.samples_to_device(S), M.samples_to_device(T)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(w["epochs"]):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+        oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
+    got, want = M.rmse(dT), oracle.rmse(Po, Qo, T)
+    print(f"tiny hogwild rmse gpu={got:.6f} oracle={want:.6f}")
+    assert abs(got - want) <= tol
+
+
+# ---------------------------------------------------------------------------- errors
+def test_error_paths(M):
+    import torch
+    rng = np.random.default_rng(1)
+    M.finalize()
+    S = M.samples_to_device(rand_samples(rng, 10, 10, 100))
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(S, 0.01, 0.0, 0.0)
+    assert e.value.code == M.ESTATE
+    with pytest.raises(M.MfsgdError) as e:
+        M.init(10, 10, 0, 1)
+    assert e.value.code == M.EINVAL
+    with pytest.raises(M.MfsgdError) as e:
+        M.init(0, 10, 8, 1)
+    assert e.value.code == M.EINVAL
+    setup(M, 10, 10, 8, 1)
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(S, 0.01, 0.0, 0.0, 7)
+    assert e.value.code == M.EINVAL
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(S, float("nan"), 0.0, 0.0)
+    assert e.value.code == M.EINVAL
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(S, 0.01, 0.0, 0.0, "wavefront")  # no plan
+    assert e.value.code == M.ESTATE
+    with pytest.raises(M.MfsgdError) as e:
+        M.plan(S, 65)
+    assert e.value.code == M.EINVAL
+    bad = rand_samples(rng, 10, 10, 100)
+    bad["v"][57] = 10  # one past the last item: only index checks ever see it
+    dbad = M.samples_to_device(bad)
+    with pytest.raises(M.MfsgdError) as e:
+        M.check_samples(dbad)
+    assert e.value.code == M.EINVAL
+    with pytest.raises(M.MfsgdError) as e:
+        M.plan(dbad, 2)
+    assert e.value.code == M.EINVAL
+    M.check_samples(S)
+    M.plan(S, 2)
+    M.epoch(S, 0.01, 0.0, 0.0, "wavefront")
+    M.sync()
+    # the plan belongs to its sample array
+    S2 = S.clone()
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(S2, 0.01, 0.0, 0.0, "wavefront")
+    assert e.value.code == M.ESTATE
+    # empty epochs are fine
+    M.epoch(S[:0], 0.01, 0.0, 0.0)
+    assert M.rmse(S[:0]) == 0.0
+    # diverging training is reported as a non-finite RMSE
+    M.set_factors(torch.full((10, 8), 1e30, device="cuda"), torch.full((10, 8), 1e30, device="cuda"))
+    with pytest.raises(M.MfsgdError) as e:
+        M.rmse(S)
+    assert e.value.code == M.ENUMERIC
+
+
+def test_ticket_timeout_is_reported(M):
+    """A spin limit of one poll makes the waiting teams give up (forced from the
+    host); every team leaves, the error surfaces at the next sync and the next
+    epoch runs normally."""
+    rng = np.random.default_rng(2)
+    m, n, s = 800, 800, 8
+    S = rand_samples(rng, m, n, 60_000)
+    S["u"][:50_000] = rng.integers(0, m // s, 50_000)  # row block 0 is much heavier
+    setup(M, m, n, 32, 4, spin_limit=1)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    M.epoch(dS, 0.001, 0.0, 0.0, "wavefront_det")
+    with pytest.raises(M.MfsgdError) as e:
+        M.sync()
+    assert e.value.code == M.ETIMEOUT
+    M.set_option("spin_limit", 1 << 24)
+    M.epoch(dS, 0.001, 0.0, 0.0, "wavefront_det")
+    M.sync()
