@@ -97,7 +97,8 @@ def main():
     ap.add_argument("--grid-s", type=int, default=32)
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--depth", type=int, default=4)
-    ap.add_argument("--waves-per-block", type=int, default=8)
+    ap.add_argument("--team-waves", type=int, default=0)
+    ap.add_argument("--partition", type=int, default=2, help="batch-Hogwild!: 0 one address space, 1 XCD-partitioned, 2 automatic")
     ap.add_argument("--ntrain", type=int, default=0, help="override the training size (0: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--cpu-threads", type=int, default=16)
@@ -131,10 +132,12 @@ def main():
     dtype = 1 if w["dtype"] == "fp16" else 0
     feat_bytes = 2 if dtype else 4
     for key, val in dict(dtype=dtype, batch_f=256, workers=args.workers, depth=args.depth,
-                         waves_per_block=args.waves_per_block, debug=0).items():
+                         team_waves=args.team_waves, partition=args.partition, debug=0).items():
         mfsgd.set_option(key, val)
     mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
     resident = mfsgd.get_option("resident_waves")
+    partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1
+    kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
     if args.scheme != "hogwild":
         t0 = time.perf_counter()
         mfsgd.plan(dS, args.grid_s)
@@ -179,7 +182,7 @@ def main():
     avg_epoch_s = sum(epoch_ms) / len(epoch_ms) / 1e3
     achieved_gbs = nnz * bytes_per_update / avg_epoch_s / 1e9
     value = nnz * args.steps / wall
-    key = f"{args.scheme}_{w['name']}"
+    key = f"{kernel}_{args.scheme}_{w['name']}"
     traffic = measured_traffic(key)
     out = {
         "metric": "SGD updates/sec and achieved HBM GB/s (% of peak) at k=128, 1 MI355X",
@@ -196,11 +199,12 @@ def main():
         "data": "synthetic (planted low-rank model with the Netflix shape, seeded)",
         "config": {"workload": f"{w['name']}: m={w['m']} n={w['n']} k={w['k']} nnz={nnz} ntest={len(T)} "
                                f"{w['dtype']} {args.scheme} f=256",
-                   "scheme": args.scheme, "workers": args.workers or "auto", "resident_waves": resident,
+                   "scheme": args.scheme, "partitioned": partitioned, "workers": args.workers or "auto",
+                   "resident_waves": resident,
                    "depth": args.depth, "epochs_timed": args.steps},
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_hogwild" if args.scheme == "hogwild" else "k_wavefront",
+                     "kernel": kernel,
                      "bytes_per_update": bytes_per_update, "updates_per_launch": nnz,
                      "avg_launch_ms": avg_epoch_s * 1e3},
         "epoch_updates_per_s": nnz / avg_epoch_s,

@@ -57,21 +57,37 @@ enum {
     MFSGD_ENUMERIC = -6  /* non-finite RMSE                                 */
 };
 
-/* Schedules (section 3.2). */
+/* Schedules (section 3.2).
+ *
+ * MI355X has eight XCDs, each with its own L2 cache; the L2s are not coherent
+ * with each other inside a kernel.  Lock-free updates that meet in one L2 see
+ * each other at once; updates from different XCDs only when lines are
+ * written back and evicted.  The block-scheduled forms keep each worker team
+ * on one XCD and pass rows between teams only at block hand-over (agent-scope
+ * release/acquire), which is the paper's own answer for workers without a
+ * shared coherent memory (section 2.3, and the block partition of section
+ * 4.1 applied to XCDs instead of GPUs). */
 enum {
-    /* batch-Hogwild! (section 3.2.2): the sample array is cut into batches
-     * of f consecutive samples; batch b goes to worker b mod W, which updates
-     * its batches in increasing order, each sample in array order; workers
-     * do not lock.  One worker is one 64-lane wavefront. */
+    /* batch-Hogwild! (section 3.2.2): samples are taken in batches of f
+     * consecutive samples, each batch updated serially by one worker, workers
+     * never lock.  With option "partition" = 0 the whole array is
+     * split into batches, batch b going to worker (wavefront) b mod W, over
+     * the whole GPU in one address space: updates made on one XCD reach the
+     * others as lines are written back and evicted (see "sync_every").  With
+     * "partition" = 1 the rating matrix is cut into an s x s grid (s = number
+     * of XCDs unless "hogwild_grid" says otherwise; planned internally, once
+     * per sample array) and one team of wavefronts per XCD runs
+     * batch-Hogwild! inside the block the wavefront schedule below gives it,
+     * so concurrent updates always meet in one L2. */
     MFSGD_BATCH_HOGWILD = 0,
     /* wavefront-update (section 3.2.3) on the s x s grid of the last
      * mfsgd_plan: worker i owns row block i and visits the column blocks in
      * the order sigma_i(w) = C[(i + O[w]) mod s], C and O permutations drawn
-     * per epoch, so the blocks of one wave share no row and no column.  A
-     * 1-D array of column tickets orders the waves: worker i starts wave w
-     * once column sigma_i(w) has been released by wave w-1.  A worker is a
-     * team of `waves_per_block` wavefronts that run batch-Hogwild! inside
-     * the block. */
+     * per epoch from (seed, epoch), so the blocks of one wave share no row and
+     * no column.  A 1-D array of column tickets orders the waves: worker i
+     * starts wave w once column sigma_i(w) has been released by wave w-1.  A
+     * worker is a team of "team_waves" wavefronts on one XCD running
+     * batch-Hogwild! inside the block. */
     MFSGD_WAVEFRONT = 1,
     /* the same schedule with one wavefront per worker and each block's
      * samples in their array order: the result then equals the serial
@@ -82,26 +98,51 @@ enum {
 enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
 
 /* Options (integer valued).  Keys:
- *   "dtype"           feature storage: MFSGD_FP32 (default) or MFSGD_FP16
- *                     (binary16 storage, binary32 arithmetic, round to
- *                     nearest even on store; section 3.1 "Half-precision").
- *                     Takes effect at the next mfsgd_init.
- *   "batch_f"         batch size f of batch-Hogwild!, a positive multiple of
- *                     64 (default 256, the paper's choice in section 3.2.2).
- *   "workers"         batch-Hogwild! worker count W (wavefronts); 0 = as many
- *                     as the GPU holds resident (default 0).
- *   "depth"           samples each wavefront keeps in flight: 1, 2, 4 or 8
- *                     (default 4).  A wavefront forwards its own pending
- *                     updates, so depth never changes the serial semantics
- *                     of one worker.
- *   "waves_per_block" wavefronts per wavefront-update worker, 1..16
- *                     (default 8).
- *   "spin_limit"      polls of a column ticket before the wait gives up with
- *                     MFSGD_ETIMEOUT (default 2^24, each poll sleeps briefly).
- *   "debug"           bit 0: count visits of every sample (read with
- *                     mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
- *                     schedule (MFSGD_DBG_TRACE).  Takes effect at the next
- *                     epoch; costs one extra atomic per sample.
+ *   "dtype"        feature storage: MFSGD_FP32 (default) or MFSGD_FP16
+ *                  (binary16 storage, binary32 arithmetic, round to nearest
+ *                  even on store; section 3.1 "Half-precision").  Takes
+ *                  effect at the next mfsgd_init.
+ *   "batch_f"      batch size f, a positive multiple of 64 (default 256, the
+ *                  paper's choice in section 3.2.2).
+ *   "workers"      batch-Hogwild! wavefronts in total; 0 (default) = as many
+ *                  as stay resident on the GPU.
+ *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8
+ *                  (default 4).  A wavefront forwards its own pending
+ *                  updates, so depth never changes the serial semantics of
+ *                  one worker.
+ *   "team_waves"   wavefronts per wavefront-update worker; 0 (default) = as
+ *                  many as stay resident, divided over the s workers.
+ *   "partition"    batch-Hogwild!: 0 one address space, 1 partitioned over
+ *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
+ *                  partitioned when P and Q together take at most 64 MiB
+ *                  (they would otherwise sit in every XCD's L2 for the whole
+ *                  epoch as diverging copies), one address space above that.
+ *   "hogwild_grid" grid side of the partitioned batch-Hogwild!; 0 (default)
+ *                  = number of XCDs.
+ *   "balance"      how a grid is cut: 1 (default) into consecutive index
+ *                  ranges holding as equal sample counts as consecutive
+ *                  ranges allow (the smallest possible largest range, ranges
+ *                  filled greedily at that size); 0 into equal index ranges
+ *                  floor(u*s/m), floor(v*s/n).
+ *   "sync_every"   one-address-space batch-Hogwild!: every this many of its
+ *                  batches, one wavefront per XCD writes that XCD's L2 back
+ *                  and invalidates it, bounding how long an update stays
+ *                  invisible to other XCDs; 0 (default) = never.
+ *   "sync_l1"      with sync_every: the other wavefronts also drop their CU's
+ *                  L1 at those points (default 0).
+ *   "spin_limit"   polls of a column ticket before the wait gives up with
+ *                  MFSGD_ETIMEOUT (default 2^24, each poll sleeps briefly).
+ *   "debug"        bit 0: count visits of every sample (read with
+ *                  mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
+ *                  schedule (MFSGD_DBG_TRACE).  Costs one extra atomic per
+ *                  sample; a block-scheduled epoch needs a plan made while
+ *                  bit 0 was set.
+ * Read-only keys (after mfsgd_init): "resident_waves" (wavefronts of the
+ * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs the
+ * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
+ * "partitioned" (whether batch-Hogwild! runs partitioned for this model),
+ * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
+ * block-scheduled kernel).
  * Returns MFSGD_EINVAL for an unknown key or an out-of-range value. */
 int mfsgd_set_option(const char* key, int64_t value);
 int mfsgd_get_option(const char* key, int64_t* value);
@@ -118,24 +159,25 @@ int mfsgd_get_option(const char* key, int64_t* value);
 int mfsgd_init(int64_t m, int64_t n, int32_t k, uint64_t seed);
 
 /* Wavefront-update preparation (section 3.2.3): check every sample's indices
- * (0 <= u < m, 0 <= v < n), cut the grid into s x s blocks (row block
- * floor(u*s/m), column block floor(v*s/n)) and keep a library-owned copy of
- * the samples grouped by block, in array order inside each block.  The plan
- * is tied to (samples, nnz): a wavefront epoch on other samples returns
- * MFSGD_ESTATE.  Synchronises `stream`.
- * EINVAL: s not in [1, 64], nnz < 0, NULL samples with nnz > 0, or an
- * out-of-range index (nothing is planned then). */
+ * (0 <= u < m, 0 <= v < n), cut the grid into s x s blocks (see option
+ * "balance") and keep a library-owned copy of the samples grouped by block,
+ * in array order inside each block.  The plan is tied to (samples, nnz): a
+ * wavefront epoch on other samples returns MFSGD_ESTATE.  Synchronises
+ * `stream`.  EINVAL: s not in [1, 64], nnz < 0, NULL samples with nnz > 0,
+ * or an out-of-range index (nothing is planned then). */
 int mfsgd_plan(const mfsgd_sample* samples, int64_t nnz, int32_t s, void* stream);
 
 /* One epoch: every one of the nnz samples is used for exactly one update
  * (section 2.3), under `scheme`, with learning rate lr and regularisation
- * lambda_p, lambda_q (section 2.2).  Asynchronous on `stream`; increments
- * the epoch counter, which keys the wavefront column orders.  Indices are
- * not checked here (use mfsgd_check_samples or mfsgd_plan): an index out of
- * range is undefined behaviour.
+ * lambda_p, lambda_q (section 2.2).  Asynchronous on `stream`, except that
+ * the first partitioned batch-Hogwild! epoch on a sample array plans it
+ * (synchronously, like mfsgd_plan).  Increments the epoch counter, which
+ * keys the per-epoch column orders.  Indices are not checked by the
+ * one-address-space batch-Hogwild! (use mfsgd_check_samples): an index out
+ * of range is undefined behaviour there.
  * EINVAL: nnz < 0, NULL samples with nnz > 0, unknown scheme, non-finite lr
- * or lambda.  ESTATE: no init, or a wavefront scheme without a plan for
- * these samples. */
+ * or lambda, or (planning) an index out of range.  ESTATE: no init, or a
+ * wavefront scheme without a plan for these samples. */
 int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
                 int32_t scheme, void* stream);
 

@@ -68,10 +68,14 @@ def lib():
         L.orc_fisher_yates.restype = None
         L.orc_wavefront_sigma.argtypes = [u64, i64, i32, vp]
         L.orc_wavefront_sigma.restype = C.c_int
-        L.orc_block_order.argtypes = [vp, i64, i64, i64, i32, vp, vp]
+        L.orc_balanced_bounds.argtypes = [vp, i64, i64, C.c_int, i32, vp]
+        L.orc_balanced_bounds.restype = C.c_int
+        L.orc_bounded_block.argtypes = [i64, vp, i32]
+        L.orc_bounded_block.restype = i32
+        L.orc_block_order.argtypes = [vp, i64, i64, i64, i32, vp, vp, vp, vp]
         L.orc_block_order.restype = C.c_int
         L.orc_epoch_wavefront.argtypes = [i64, i64, i32, C.c_int, vp, vp, vp, i64, f32, f32, f32, i32, u64,
-                                          i64]
+                                          i64, C.c_int]
         L.orc_epoch_wavefront.restype = C.c_int
         L.orc_rmse.argtypes = [i32, C.c_int, vp, vp, vp, i64]
         L.orc_rmse.restype = f64
@@ -143,11 +147,12 @@ def epoch_serial(P, Qt, S, lr, lambda_p, lambda_q):
         raise MemoryError("oracle epoch failed")
 
 
-def epoch_wavefront(P, Qt, S, lr, lambda_p, lambda_q, s, seed, t):
-    """In place: one deterministic wavefront-update epoch (serial-equivalent order)."""
+def epoch_wavefront(P, Qt, S, lr, lambda_p, lambda_q, s, seed, t, balanced=False):
+    """In place: one deterministic wavefront-update epoch (serial-equivalent order).
+    balanced: cut the grid by sample counts (balanced_bounds) instead of equal index ranges."""
     S = _samples(S)
     rc = lib().orc_epoch_wavefront(P.shape[0], Qt.shape[0], P.shape[1], _dtype_code(P), _ptr(P), _ptr(Qt),
-                                   _ptr(S), len(S), lr, lambda_p, lambda_q, s, seed, t)
+                                   _ptr(S), len(S), lr, lambda_p, lambda_q, s, seed, t, int(bool(balanced)))
     if rc:
         raise MemoryError("oracle wavefront epoch failed")
 
@@ -188,11 +193,29 @@ def col_block(v, n, s):
     return lib().orc_col_block(v, n, s)
 
 
-def block_order(S, m, n, s):
+def balanced_bounds(S, N, which, s) -> np.ndarray:
+    """First index of each of the s consecutive ranges (which: 0 users, 1 items)
+    whose largest sample count is minimal; bounds[s] = N."""
+    S = _samples(S)
+    b = np.empty(s + 1, dtype=np.int64)
+    if lib().orc_balanced_bounds(_ptr(S), len(S), N, which, s, _ptr(b)):
+        raise MemoryError
+    return b
+
+
+def bounded_block(i, bounds, s) -> int:
+    b = np.ascontiguousarray(bounds, dtype=np.int64)
+    return lib().orc_bounded_block(i, _ptr(b), s)
+
+
+def block_order(S, m, n, s, balanced=False):
     S = _samples(S)
     order = np.empty(max(len(S), 1), dtype=np.int64)
     start = np.empty(s * s + 1, dtype=np.int64)
-    if lib().orc_block_order(_ptr(S), len(S), m, n, s, _ptr(order), _ptr(start)):
+    rb = balanced_bounds(S, m, 0, s) if balanced else None
+    cb = balanced_bounds(S, n, 1, s) if balanced else None
+    if lib().orc_block_order(_ptr(S), len(S), m, n, s, None if rb is None else _ptr(rb),
+                             None if cb is None else _ptr(cb), _ptr(order), _ptr(start)):
         raise MemoryError
     return order[:len(S)], start
 

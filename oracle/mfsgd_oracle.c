@@ -242,6 +242,68 @@ void orc_hogwild_batch_owner(int64_t nnz, int32_t f, int64_t W, int64_t* out)
 int32_t orc_row_block(int64_t u, int64_t m, int32_t s) { return (int32_t)((u * (int64_t)s) / m); }
 int32_t orc_col_block(int64_t v, int64_t n, int32_t s) { return (int32_t)((v * (int64_t)s) / n); }
 
+/* Load-balanced alternative to the equal index ranges above (the paper draws
+ * equal blocks and does not say how they are cut).  The indices (users if
+ * which == 0, items if which == 1) are split into s consecutive ranges so
+ * that the largest number of samples in one range is as small as possible.
+ * Canonical choice: C = the smallest cap for which filling ranges greedily
+ * (a range takes the next index while its count stays <= C) needs at most s
+ * ranges; the ranges are those of that greedy fill.  bounds[k] is the first
+ * index of range k; unused trailing ranges are empty and start at N. */
+static int64_t orc_greedy_ranges(const int64_t* cnt, int64_t N, int64_t cap, int32_t s, int64_t* bounds)
+{
+    int64_t k = 0, load = 0;
+    if (bounds)
+        bounds[0] = 0;
+    for (int64_t i = 0; i < N; i++) {
+        if (load + cnt[i] > cap) {
+            k++;
+            load = 0;
+            if (bounds && k <= s)
+                bounds[k] = i;
+        }
+        load += cnt[i];
+    }
+    if (bounds)
+        for (int64_t j = k + 1; j <= s; j++)
+            bounds[j] = N;
+    return k + 1;
+}
+
+int orc_balanced_bounds(const orc_sample* S, int64_t nnz, int64_t N, int which, int32_t s, int64_t* bounds)
+{
+    int64_t* cnt = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    if (!cnt)
+        return -2;
+    int64_t top = 0;
+    for (int64_t i = 0; i < nnz; i++)
+        cnt[which ? S[i].v : S[i].u]++;
+    for (int64_t i = 0; i < N; i++)
+        top = cnt[i] > top ? cnt[i] : top;
+    int64_t lo = (nnz + s - 1) / s;
+    lo = lo > top ? lo : top;
+    int64_t hi = nnz > lo ? nnz : lo; /* one range holding everything always fits */
+    while (lo < hi) {                 /* smallest feasible cap */
+        int64_t mid = lo + (hi - lo) / 2;
+        if (orc_greedy_ranges(cnt, N, mid, s, NULL) <= s)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    orc_greedy_ranges(cnt, N, lo, s, bounds);
+    free(cnt);
+    return 0;
+}
+
+int32_t orc_bounded_block(int64_t i, const int64_t* bounds, int32_t s)
+{
+    int32_t k = 0;
+    for (int32_t j = 0; j < s; j++)
+        if (bounds[j] <= i)
+            k = j;
+    return k;
+}
+
 /* Durstenfeld's Fisher-Yates: for i = s-1 down to 1 swap a[i] with a[j],
  * j uniform on 0..i.  Draw number (s-1-i) of the stream gives j as the high
  * 32 bits times (i+1), shifted down 32 (multiply-shift range reduction). */
@@ -282,8 +344,17 @@ int orc_wavefront_sigma(uint64_t seed, int64_t t, int32_t s, int32_t* sigma)
  * order[] receives the sample indices block by block (block id I*s+J
  * ascending), start[b] .. start[b+1] delimits block b.  A counting pass,
  * a prefix sum and an in-order placement. */
-int orc_block_order(const orc_sample* S, int64_t nnz, int64_t m, int64_t n, int32_t s, int64_t* order,
-                    int64_t* start)
+static int64_t orc_block_id(const orc_sample* x, int64_t m, int64_t n, int32_t s, const int64_t* rb,
+                            const int64_t* cb)
+{
+    int32_t r = rb ? orc_bounded_block(x->u, rb, s) : orc_row_block(x->u, m, s);
+    int32_t c = cb ? orc_bounded_block(x->v, cb, s) : orc_col_block(x->v, n, s);
+    return (int64_t)r * s + c;
+}
+
+/* rb, cb: balanced bounds (s+1 entries each) or NULL for equal index ranges. */
+int orc_block_order(const orc_sample* S, int64_t nnz, int64_t m, int64_t n, int32_t s, const int64_t* rb,
+                    const int64_t* cb, int64_t* order, int64_t* start)
 {
     int64_t nb = (int64_t)s * s;
     int64_t* fill = (int64_t*)calloc((size_t)nb, sizeof(int64_t));
@@ -291,14 +362,12 @@ int orc_block_order(const orc_sample* S, int64_t nnz, int64_t m, int64_t n, int3
         return -2;
     for (int64_t b = 0; b <= nb; b++)
         start[b] = 0;
-    for (int64_t i = 0; i < nnz; i++) {
-        int64_t b = (int64_t)orc_row_block(S[i].u, m, s) * s + orc_col_block(S[i].v, n, s);
-        start[b + 1]++;
-    }
+    for (int64_t i = 0; i < nnz; i++)
+        start[orc_block_id(&S[i], m, n, s, rb, cb) + 1]++;
     for (int64_t b = 0; b < nb; b++)
         start[b + 1] += start[b];
     for (int64_t i = 0; i < nnz; i++) {
-        int64_t b = (int64_t)orc_row_block(S[i].u, m, s) * s + orc_col_block(S[i].v, n, s);
+        int64_t b = orc_block_id(&S[i], m, n, s, rb, cb);
         order[start[b] + fill[b]++] = i;
     }
     free(fill);
@@ -311,15 +380,21 @@ int orc_block_order(const orc_sample* S, int64_t nnz, int64_t m, int64_t n, int3
  * inside a block, array order. */
 int orc_epoch_wavefront(int64_t m, int64_t n, int32_t k, int dtype, void* P, void* Qt, const orc_sample* S,
                         int64_t nnz, float lr, float lambda_p, float lambda_q, int32_t s, uint64_t seed,
-                        int64_t t)
+                        int64_t t, int balanced)
 {
     int64_t nb = (int64_t)s * s;
     int64_t* order = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nnz > 0 ? nnz : 1));
     int64_t* start = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nb + 1));
     int32_t* sigma = (int32_t*)malloc(sizeof(int32_t) * (size_t)nb);
     double* buf = (double*)malloc(2 * sizeof(double) * (size_t)k);
+    int64_t* rb = (int64_t*)malloc(sizeof(int64_t) * (size_t)(s + 1));
+    int64_t* cb = (int64_t*)malloc(sizeof(int64_t) * (size_t)(s + 1));
     int rc = -2;
-    if (order && start && sigma && buf && orc_block_order(S, nnz, m, n, s, order, start) == 0 &&
+    if (balanced && rb && cb &&
+        (orc_balanced_bounds(S, nnz, m, 0, s, rb) || orc_balanced_bounds(S, nnz, n, 1, s, cb)))
+        balanced = -1;
+    if (balanced >= 0 && order && start && sigma && buf && rb && cb &&
+        orc_block_order(S, nnz, m, n, s, balanced ? rb : NULL, balanced ? cb : NULL, order, start) == 0 &&
         orc_wavefront_sigma(seed, t, s, sigma) == 0) {
         for (int32_t w = 0; w < s; w++)
             for (int32_t i = 0; i < s; i++) {
@@ -333,6 +408,8 @@ int orc_epoch_wavefront(int64_t m, int64_t n, int32_t k, int dtype, void* P, voi
     free(start);
     free(sigma);
     free(buf);
+    free(rb);
+    free(cb);
     return rc;
 }
 

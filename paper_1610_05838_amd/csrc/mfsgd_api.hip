@@ -1,10 +1,12 @@
 // mfsgd_api.hip -- the C ABI (include/mfsgd.h): context, argument checks,
-// buffer ownership, kernel selection and device-error reporting.
+// buffer ownership, plans, team layout, kernel selection and device-error
+// reporting.
+#include <algorithm>
 #include <cmath>
-#include <cstdio>
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "mfsgd.h"
 #include "mfsgd_device.hpp"
@@ -21,41 +23,63 @@ struct Options {
     int64_t batch_f = 256;
     int64_t workers = 0;
     int64_t depth = 4;
-    int64_t waves_per_block = 8;
+    int64_t team_waves = 0;
+    int64_t partition = 2;
+    int64_t hogwild_grid = 0;
+    int64_t balance = 1;
+    int64_t sync_every = 0;
+    int64_t sync_l1 = 0;
     int64_t spin_limit = int64_t(1) << 24;
     int64_t debug = 0;
+};
+
+// A grouping of one sample array into the blocks of an s x s grid.
+struct Plan {
+    const mfsgd_sample* src = nullptr;
+    int64_t nnz = -1;
+    int s = 0;
+    bool balanced = false;
+    bool has_orig = false;
+    Sample* Sp = nullptr;
+    int64_t Sp_cap = 0;
+    int64_t* orig = nullptr;
+    int64_t orig_cap = 0;
+    int64_t* bstart = nullptr; // kMaxGrid^2 + 1
+    bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
+    void invalidate()
+    {
+        src = nullptr;
+        nnz = -1;
+    }
 };
 
 struct Context {
     bool inited = false;
     int device = 0;
     int cus = 0;
+    int nx = 1; // XCDs workgroups are dealt to round-robin (1 if not that layout)
     int64_t m = 0, n = 0;
     int k = 0, KP = 0, dtype = 0;
     uint64_t seed = 0;
     int64_t epoch = 0;
     void* P = nullptr;
     void* Q = nullptr;
-    // small device/pinned buffers
     uint32_t* tickets = nullptr;
+    uint32_t* done = nullptr;
     int* err = nullptr;
     int* bad = nullptr;
     double* partial = nullptr;
     double* dres = nullptr;
     double* hres = nullptr; // pinned
     int* hflag = nullptr;   // pinned
-    // plan
-    const mfsgd_sample* plan_src = nullptr;
-    int64_t plan_nnz = -1;
-    int plan_s = 0;
-    bool plan_orig = false;
-    Sample* Sp = nullptr;
-    int64_t Sp_cap = 0;
-    int64_t* orig = nullptr;
-    int64_t orig_cap = 0;
+    Plan wf;                // the caller's wavefront-update plan (mfsgd_plan)
+    Plan hw;                // internal plan of the XCD-partitioned batch-Hogwild!
+    // planner scratch
     int32_t* counts = nullptr;
     int64_t* totals = nullptr;
-    int64_t* bstart = nullptr;
+    int64_t* bnd = nullptr; // 2 x (kMaxGrid + 1)
+    uint32_t* deg = nullptr;
+    int64_t deg_cap = 0;
     // debug
     uint32_t* visits = nullptr;
     int64_t visits_cap = 0, visits_n = 0;
@@ -79,6 +103,13 @@ int fail(int code, const std::string& msg)
             return fail(MFSGD_EHIP, std::string(#call) + ": " + hipGetErrorString(e_));                          \
     } while (0)
 
+#define CHK(expr)                                                                                                  \
+    do {                                                                                                           \
+        int rc_ = (expr);                                                                                          \
+        if (rc_ != MFSGD_OK)                                                                                       \
+            return rc_;                                                                                            \
+    } while (0)
+
 template <typename F>
 int guarded(F&& f)
 {
@@ -92,11 +123,10 @@ int guarded(F&& f)
     }
 }
 
-int dfree(void* p)
+void dfree(void* p)
 {
     if (p)
         (void)hipFree(p);
-    return 0;
 }
 
 int dalloc(void** p, size_t bytes, const char* what)
@@ -128,12 +158,21 @@ int grow(T** p, int64_t* cap, int64_t need, const char* what)
     return rc;
 }
 
+void free_plan(Plan& p)
+{
+    dfree(p.Sp);
+    dfree(p.orig);
+    dfree(p.bstart);
+    p = Plan();
+}
+
 void release_all()
 {
     Context& c = g;
     dfree(c.P);
     dfree(c.Q);
     dfree(c.tickets);
+    dfree(c.done);
     dfree(c.err);
     dfree(c.bad);
     dfree(c.partial);
@@ -142,11 +181,12 @@ void release_all()
         (void)hipHostFree(c.hres);
     if (c.hflag)
         (void)hipHostFree(c.hflag);
-    dfree(c.Sp);
-    dfree(c.orig);
+    free_plan(c.wf);
+    free_plan(c.hw);
     dfree(c.counts);
     dfree(c.totals);
-    dfree(c.bstart);
+    dfree(c.bnd);
+    dfree(c.deg);
     dfree(c.visits);
     dfree(c.trace);
     c = Context();
@@ -172,6 +212,12 @@ int occupancy_waves(int KP, int dtype, int depth)
     return dtype == MFSGD_FP16 ? occupancy_f16(KP, depth) : occupancy_f32(KP, depth);
 }
 
+int occupancy_blocked(int KP, int dtype, int depth, int threads)
+{
+    return dtype == MFSGD_FP16 ? occupancy_blocked_f16(KP, depth, threads)
+                               : occupancy_blocked_f32(KP, depth, threads);
+}
+
 // Read back and clear the device error flag; the stream has been synchronised.
 int take_device_error()
 {
@@ -179,7 +225,7 @@ int take_device_error()
         *g.hflag = 0;
         int zero = 0;
         HIPCHK(hipMemcpy(g.err, &zero, sizeof(int), hipMemcpyHostToDevice));
-        return fail(MFSGD_ETIMEOUT, "a wavefront-update ticket wait exceeded spin_limit; the epoch was abandoned");
+        return fail(MFSGD_ETIMEOUT, "a block-schedule ticket wait exceeded spin_limit; the epoch was abandoned");
     }
     return MFSGD_OK;
 }
@@ -193,70 +239,117 @@ int sync_and_check(hipStream_t st)
 
 bool valid_samples(const mfsgd_sample* s, int64_t nnz) { return nnz >= 0 && (nnz == 0 || s != nullptr); }
 
+// Whether batch-Hogwild! runs partitioned over the XCDs.  Automatic choice:
+// when both factor matrices fit in kPartitionBytes they stay resident in every
+// XCD's L2 for the whole epoch, so one-address-space workers would train eight
+// diverging copies; partitioned teams keep every update in one L2.  Larger
+// models are evicted quickly enough that the one-address-space form stays
+// close to it and runs faster.
+constexpr int64_t kPartitionBytes = int64_t(64) << 20;
+
+bool partitioned_hogwild()
+{
+    if (g_opt.partition != 2)
+        return g_opt.partition == 1;
+    const int64_t model = (g.m + g.n) * (int64_t)g.KP * (int64_t)elem_size(g.dtype);
+    return model <= kPartitionBytes;
+}
+
+// ---------------------------------------------------------------------------
+// options
+// ---------------------------------------------------------------------------
+struct OptSpec {
+    const char* key;
+    int64_t Options::*field;
+    int64_t lo, hi;
+    const char* what;
+};
+
+const OptSpec kOpts[] = {
+    {"dtype", &Options::dtype, 0, 1, "dtype must be 0 (fp32) or 1 (fp16)"},
+    {"batch_f", &Options::batch_f, 64, int64_t(1) << 30, "batch_f must be a positive multiple of 64"},
+    {"workers", &Options::workers, 0, int64_t(1) << 30, "workers must be in [0, 2^30]"},
+    {"depth", &Options::depth, 1, 8, "depth must be 1, 2, 4 or 8"},
+    {"team_waves", &Options::team_waves, 0, 65536, "team_waves must be in [0, 65536]"},
+    {"partition", &Options::partition, 0, 2, "partition must be 0, 1 or 2"},
+    {"hogwild_grid", &Options::hogwild_grid, 0, kMaxGrid, "hogwild_grid must be in [0, 64]"},
+    {"balance", &Options::balance, 0, 1, "balance must be 0 or 1"},
+    {"sync_every", &Options::sync_every, 0, int64_t(1) << 30, "sync_every must be in [0, 2^30]"},
+    {"sync_l1", &Options::sync_l1, 0, 1, "sync_l1 must be 0 or 1"},
+    {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
+    {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
+};
+
 int set_option_impl(const char* key, int64_t value)
 {
     if (!key)
         return fail(MFSGD_EINVAL, "option key is NULL");
-    std::string k(key);
-    if (k == "dtype") {
-        if (value != MFSGD_FP32 && value != MFSGD_FP16)
-            return fail(MFSGD_EINVAL, "dtype must be 0 (fp32) or 1 (fp16)");
-        g_opt.dtype = value;
-    } else if (k == "batch_f") {
-        if (value <= 0 || value % 64 != 0 || value > (int64_t(1) << 30))
-            return fail(MFSGD_EINVAL, "batch_f must be a positive multiple of 64");
-        g_opt.batch_f = value;
-    } else if (k == "workers") {
-        if (value < 0 || value > (int64_t(1) << 30))
-            return fail(MFSGD_EINVAL, "workers must be in [0, 2^30]");
-        g_opt.workers = value;
-    } else if (k == "depth") {
-        if (value != 1 && value != 2 && value != 4 && value != 8)
-            return fail(MFSGD_EINVAL, "depth must be 1, 2, 4 or 8");
-        g_opt.depth = value;
-    } else if (k == "waves_per_block") {
-        if (value < 1 || value > 16)
-            return fail(MFSGD_EINVAL, "waves_per_block must be in [1, 16]");
-        g_opt.waves_per_block = value;
-    } else if (k == "spin_limit") {
-        if (value < 1 || value > 0xffffffffll)
-            return fail(MFSGD_EINVAL, "spin_limit must be in [1, 2^32-1]");
-        g_opt.spin_limit = value;
-    } else if (k == "debug") {
-        if (value < 0 || value > 3)
-            return fail(MFSGD_EINVAL, "debug must be in [0, 3]");
-        g_opt.debug = value;
-    } else {
-        return fail(MFSGD_EINVAL, "unknown option '" + k + "'");
+    for (const OptSpec& o : kOpts) {
+        if (std::strcmp(key, o.key) != 0)
+            continue;
+        bool ok = value >= o.lo && value <= o.hi;
+        if (ok && o.field == &Options::batch_f)
+            ok = value % 64 == 0;
+        if (ok && o.field == &Options::depth)
+            ok = value == 1 || value == 2 || value == 4 || value == 8;
+        if (!ok)
+            return fail(MFSGD_EINVAL, o.what);
+        g_opt.*(o.field) = value;
+        return MFSGD_OK;
     }
-    return MFSGD_OK;
+    return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
 }
 
 int get_option_impl(const char* key, int64_t* value)
 {
     if (!key || !value)
         return fail(MFSGD_EINVAL, "NULL argument");
-    std::string k(key);
-    if (k == "dtype")
-        *value = g_opt.dtype;
-    else if (k == "batch_f")
-        *value = g_opt.batch_f;
-    else if (k == "workers")
-        *value = g_opt.workers;
-    else if (k == "depth")
-        *value = g_opt.depth;
-    else if (k == "waves_per_block")
-        *value = g_opt.waves_per_block;
-    else if (k == "spin_limit")
-        *value = g_opt.spin_limit;
-    else if (k == "debug")
-        *value = g_opt.debug;
-    else if (k == "resident_waves") { // read-only: wavefronts of the epoch kernel the GPU holds at once
-        if (!g.inited)
-            return fail(MFSGD_ESTATE, "resident_waves needs mfsgd_init");
+    for (const OptSpec& o : kOpts)
+        if (std::strcmp(key, o.key) == 0) {
+            *value = g_opt.*(o.field);
+            return MFSGD_OK;
+        }
+    const bool ro = !std::strcmp(key, "resident_waves") || !std::strcmp(key, "xcds") || !std::strcmp(key, "cus") ||
+                    !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned");
+    if (!ro)
+        return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
+    if (!g.inited)
+        return fail(MFSGD_ESTATE, std::string("'") + key + "' is read-only and needs mfsgd_init");
+    if (!std::strcmp(key, "resident_waves"))
         *value = (int64_t)g.cus * occupancy_waves(g.KP, g.dtype, (int)g_opt.depth);
-    } else
-        return fail(MFSGD_EINVAL, "unknown option '" + k + "'");
+    else if (!std::strcmp(key, "xcds"))
+        *value = g.nx;
+    else if (!std::strcmp(key, "blocked_per_cu"))
+        *value = occupancy_blocked(g.KP, g.dtype, (int)g_opt.depth, 256);
+    else if (!std::strcmp(key, "partitioned"))
+        *value = partitioned_hogwild() ? 1 : 0;
+    else
+        *value = g.cus;
+    return MFSGD_OK;
+}
+
+// ---------------------------------------------------------------------------
+// init
+// ---------------------------------------------------------------------------
+int detect_xcds(Context& c)
+{
+    // Deal 64 workgroups and read which XCD each runs on; round-robin dealing
+    // (workgroup b on XCD b mod nx) is what the team layout relies on.
+    constexpr int kProbe = 64;
+    int* dev = nullptr;
+    CHK(dalloc((void**)&dev, sizeof(int) * kProbe, "xcd probe"));
+    std::vector<int> host(kProbe, -1);
+    hipError_t e = probe_xcc(dev, kProbe, nullptr);
+    if (e == hipSuccess)
+        e = hipMemcpy(host.data(), dev, sizeof(int) * kProbe, hipMemcpyDeviceToHost);
+    dfree(dev);
+    if (e != hipSuccess)
+        return fail(MFSGD_EHIP, std::string("XCD probe: ") + hipGetErrorString(e));
+    const int nx = 1 + *std::max_element(host.begin(), host.end());
+    bool round_robin = nx >= 1 && nx <= kMaxGrid;
+    for (int b = 0; round_robin && b < kProbe; ++b)
+        round_robin = host[b] == b % nx;
+    c.nx = round_robin ? nx : 1;
     return MFSGD_OK;
 }
 
@@ -281,9 +374,11 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     int rc;
     if ((rc = dalloc(&c.P, (size_t)m * c.KP * es, "P")) || (rc = dalloc(&c.Q, (size_t)n * c.KP * es, "Q")) ||
         (rc = dalloc((void**)&c.tickets, sizeof(uint32_t) * kMaxGrid, "tickets")) ||
+        (rc = dalloc((void**)&c.done, sizeof(uint32_t) * kMaxGrid * kMaxGrid, "team counters")) ||
         (rc = dalloc((void**)&c.err, sizeof(int), "flag")) || (rc = dalloc((void**)&c.bad, sizeof(int), "flag")) ||
         (rc = dalloc((void**)&c.partial, sizeof(double) * kRmseWaves, "rmse partials")) ||
-        (rc = dalloc((void**)&c.dres, sizeof(double), "rmse result"))) {
+        (rc = dalloc((void**)&c.dres, sizeof(double), "rmse result")) ||
+        (rc = dalloc((void**)&c.bnd, sizeof(int64_t) * 2 * (kMaxGrid + 1), "plan bounds"))) {
         release_all();
         return rc;
     }
@@ -296,7 +391,7 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     *c.hflag = 0;
     HIPCHK(hipMemset(c.err, 0, sizeof(int)));
     HIPCHK(hipMemset(c.bad, 0, sizeof(int)));
-    HIPCHK(hipMemset(c.tickets, 0, sizeof(uint32_t) * kMaxGrid));
+    HIPCHK(reset_tickets(c.tickets, c.done, nullptr));
     const double inv_sqrt_k = 1.0 / std::sqrt((double)k);
     const uint64_t sp = sm64_at(seed, kTagP), sq = sm64_at(seed, kTagQ);
     if (c.dtype == MFSGD_FP16) {
@@ -306,9 +401,126 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
         HIPCHK(init_f32(c.P, m, k, c.KP, sp, inv_sqrt_k, nullptr));
         HIPCHK(init_f32(c.Q, n, k, c.KP, sq, inv_sqrt_k, nullptr));
     }
+    CHK(detect_xcds(c));
     HIPCHK(hipDeviceSynchronize());
     c.inited = true;
     return MFSGD_OK;
+}
+
+// ---------------------------------------------------------------------------
+// plans
+// ---------------------------------------------------------------------------
+// Optimal consecutive cut of per-index counts into s ranges: the smallest cap
+// on a range's count for which a greedy fill needs at most s ranges, and the
+// ranges of that greedy fill.
+int64_t greedy_ranges(const std::vector<uint32_t>& cnt, int64_t cap, int s, int64_t* bounds)
+{
+    const int64_t N = (int64_t)cnt.size();
+    int64_t k = 0, load = 0;
+    if (bounds)
+        bounds[0] = 0;
+    for (int64_t i = 0; i < N; ++i) {
+        if (load + cnt[i] > cap) {
+            ++k;
+            load = 0;
+            if (bounds && k <= s)
+                bounds[k] = i;
+        }
+        load += cnt[i];
+    }
+    if (bounds)
+        for (int64_t j = k + 1; j <= s; ++j)
+            bounds[j] = N;
+    return k + 1;
+}
+
+void balanced_cut(const std::vector<uint32_t>& cnt, int64_t nnz, int s, int64_t* bounds)
+{
+    int64_t top = 0;
+    for (uint32_t x : cnt)
+        top = std::max<int64_t>(top, x);
+    int64_t lo = std::max<int64_t>((nnz + s - 1) / s, top);
+    int64_t hi = std::max<int64_t>(nnz, lo);
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (greedy_ranges(cnt, mid, s, nullptr) <= s)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    greedy_ranges(cnt, lo, s, bounds);
+}
+
+int bad_index_error()
+{
+    return fail(MFSGD_EINVAL, "a sample index is out of range (need 0 <= u < m and 0 <= v < n)");
+}
+
+int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool balanced, bool keep_orig,
+               hipStream_t st)
+{
+    Context& c = g;
+    pl.invalidate();
+    if (!c.counts) {
+        CHK(dalloc((void**)&c.counts, sizeof(int32_t) * kMaxGrid * kMaxGrid * kPlanChunks, "plan counts"));
+        CHK(dalloc((void**)&c.totals, sizeof(int64_t) * kMaxGrid * kMaxGrid, "plan totals"));
+    }
+    if (!pl.bstart)
+        CHK(dalloc((void**)&pl.bstart, sizeof(int64_t) * (kMaxGrid * kMaxGrid + 1), "plan starts"));
+    CHK(grow(&pl.Sp, &pl.Sp_cap, nnz, "planned samples"));
+    if (keep_orig)
+        CHK(grow(&pl.orig, &pl.orig_cap, nnz, "plan positions"));
+    const Sample* S = (const Sample*)samples;
+    HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
+    const int64_t* rbnd = nullptr;
+    const int64_t* cbnd = nullptr;
+    if (balanced) {
+        CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
+        HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(uint32_t) * (size_t)(c.m + c.n), st));
+        HIPCHK(plan_degrees(S, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
+        std::vector<uint32_t> du((size_t)c.m), dv((size_t)c.n);
+        HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(uint32_t) * du.size(), hipMemcpyDeviceToHost, st));
+        HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(uint32_t) * dv.size(), hipMemcpyDeviceToHost, st));
+        HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
+        HIPCHK(hipStreamSynchronize(st));
+        if (*c.hflag) {
+            *c.hflag = 0;
+            return bad_index_error();
+        }
+        std::vector<int64_t> b(2 * (kMaxGrid + 1));
+        balanced_cut(du, nnz, s, b.data());
+        balanced_cut(dv, nnz, s, b.data() + kMaxGrid + 1);
+        HIPCHK(hipMemcpy(c.bnd, b.data(), sizeof(int64_t) * b.size(), hipMemcpyHostToDevice));
+        rbnd = c.bnd;
+        cbnd = c.bnd + kMaxGrid + 1;
+    }
+    PlanBuffers b{c.counts, c.totals, pl.bstart, pl.Sp, keep_orig ? pl.orig : nullptr, c.bad, rbnd, cbnd};
+    HIPCHK(plan_build(S, nnz, c.m, c.n, s, b, st));
+    HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    const int bad = *c.hflag;
+    *c.hflag = 0;
+    if (bad)
+        return bad_index_error();
+    HIPCHK(plan_scatter(S, nnz, c.m, c.n, s, b, st));
+    HIPCHK(hipStreamSynchronize(st));
+    pl.src = samples;
+    pl.nnz = nnz;
+    pl.s = s;
+    pl.balanced = balanced;
+    pl.has_orig = keep_orig;
+    return MFSGD_OK;
+}
+
+int plan_impl(const mfsgd_sample* samples, int64_t nnz, int32_t s, hipStream_t st)
+{
+    if (!g.inited)
+        return fail(MFSGD_ESTATE, "mfsgd_init has not been called");
+    if (!valid_samples(samples, nnz))
+        return fail(MFSGD_EINVAL, "bad sample array");
+    if (s < 1 || s > kMaxGrid)
+        return fail(MFSGD_EINVAL, "grid side s must be in [1, 64]");
+    return build_plan(g.wf, samples, nnz, s, g_opt.balance != 0, (g_opt.debug & 1) != 0, st);
 }
 
 int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
@@ -323,53 +535,44 @@ int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
     HIPCHK(check_indices((const Sample*)samples, nnz, g.m, g.n, g.bad, st));
     HIPCHK(hipMemcpyAsync(g.hflag, g.bad, sizeof(int), hipMemcpyDeviceToHost, st));
     HIPCHK(hipStreamSynchronize(st));
-    int bad = *g.hflag;
+    const int bad = *g.hflag;
     *g.hflag = 0;
-    if (bad)
-        return fail(MFSGD_EINVAL, "a sample index is out of range (need 0 <= u < m and 0 <= v < n)");
-    return MFSGD_OK;
+    return bad ? bad_index_error() : MFSGD_OK;
 }
 
-int plan_impl(const mfsgd_sample* samples, int64_t nnz, int32_t s, hipStream_t st)
+// ---------------------------------------------------------------------------
+// epochs
+// ---------------------------------------------------------------------------
+// Team shape of a block-scheduled launch with grid side s and `want` waves per
+// team (0: as many as stay co-resident).  One-wavefront teams are single
+// workgroups placed anywhere; larger teams are workgroups of 4 wavefronts,
+// spread over the XCDs so that each team lives on one XCD.
+int team_layout(int s, int64_t want, EpochLaunch& a)
 {
     Context& c = g;
-    if (!c.inited)
-        return fail(MFSGD_ESTATE, "mfsgd_init has not been called");
-    if (!valid_samples(samples, nnz))
-        return fail(MFSGD_EINVAL, "bad sample array");
-    if (s < 1 || s > kMaxGrid)
-        return fail(MFSGD_EINVAL, "grid side s must be in [1, 64]");
-    c.plan_src = nullptr;
-    c.plan_nnz = -1;
-    int rc;
-    const int64_t nb = (int64_t)s * s;
-    if (!c.counts) {
-        if ((rc = dalloc((void**)&c.counts, sizeof(int32_t) * kMaxGrid * kMaxGrid * kPlanChunks, "plan counts")) ||
-            (rc = dalloc((void**)&c.totals, sizeof(int64_t) * kMaxGrid * kMaxGrid, "plan totals")) ||
-            (rc = dalloc((void**)&c.bstart, sizeof(int64_t) * (kMaxGrid * kMaxGrid + 1), "plan starts")))
-            return rc;
+    if (want == 1) {
+        a.nx = 1;
+        a.wg_waves = 1;
+        a.wg_per_team = 1;
+        return MFSGD_OK;
     }
-    if ((rc = grow(&c.Sp, &c.Sp_cap, nnz, "planned samples")))
-        return rc;
-    const bool keep_orig = (g_opt.debug & 1) != 0;
-    if (keep_orig && (rc = grow(&c.orig, &c.orig_cap, nnz, "plan positions")))
-        return rc;
-    PlanBuffers b{c.counts, c.totals, c.bstart, c.Sp, keep_orig ? c.orig : nullptr, c.bad};
-    HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
-    HIPCHK(plan_build((const Sample*)samples, nnz, c.m, c.n, s, b, st));
-    HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
-    HIPCHK(hipStreamSynchronize(st));
-    const int bad = *c.hflag;
-    *c.hflag = 0;
-    if (bad)
-        return fail(MFSGD_EINVAL, "a sample index is out of range (need 0 <= u < m and 0 <= v < n)");
-    HIPCHK(plan_scatter((const Sample*)samples, nnz, c.m, c.n, s, b, st));
-    HIPCHK(hipStreamSynchronize(st));
-    (void)nb;
-    c.plan_src = samples;
-    c.plan_nnz = nnz;
-    c.plan_s = s;
-    c.plan_orig = keep_orig;
+    const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 256);
+    if (per_cu <= 0)
+        return fail(MFSGD_EHIP, "occupancy query failed for the block-scheduled kernel");
+    // Every workgroup of this persistent grid must be resident at once (teams
+    // wait on each other).  Measured on MI355X, fewer workgroups fit than the
+    // occupancy query reports (about 5.3 of 7 per CU), so only half of the
+    // reported count is used; 3-4K wavefronts already saturate the memory
+    // system.  A grid that still did not fit would end in MFSGD_ETIMEOUT,
+    // not a hang.
+    const int64_t cap = (int64_t)std::max(1, per_cu / 2) * c.cus; // co-resident workgroups
+    if (cap < s)
+        return fail(MFSGD_EINVAL, "grid side exceeds the co-resident workgroup count");
+    int64_t G = want > 0 ? (want + 3) / 4 : cap / s;
+    G = std::max<int64_t>(1, std::min<int64_t>(G, cap / s));
+    a.nx = (c.nx > 1 && s % c.nx == 0) ? c.nx : 1;
+    a.wg_waves = 4;
+    a.wg_per_team = (int)G;
     return MFSGD_OK;
 }
 
@@ -385,12 +588,24 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         return fail(MFSGD_EINVAL, "lr and lambdas must be finite");
     if (scheme != MFSGD_BATCH_HOGWILD && scheme != MFSGD_WAVEFRONT && scheme != MFSGD_WAVEFRONT_DET)
         return fail(MFSGD_EINVAL, "unknown scheme");
-    const bool wavefront = scheme != MFSGD_BATCH_HOGWILD;
-    if (wavefront && (c.plan_src != samples || c.plan_nnz != nnz))
-        return fail(MFSGD_ESTATE, "wavefront-update needs mfsgd_plan on these samples first");
     const int64_t dbg = g_opt.debug;
-    if (wavefront && (dbg & 1) && !c.plan_orig)
-        return fail(MFSGD_ESTATE, "visit counting in wavefront-update needs a plan made with debug bit 0 set");
+    const bool hog = scheme == MFSGD_BATCH_HOGWILD;
+    const bool blocked = !hog || partitioned_hogwild();
+    Plan* pl = nullptr;
+    if (!hog) {
+        if (!c.wf.matches(samples, nnz))
+            return fail(MFSGD_ESTATE, "wavefront-update needs mfsgd_plan on these samples first");
+        pl = &c.wf;
+    } else if (blocked) {
+        const int s_h = g_opt.hogwild_grid > 0 ? (int)g_opt.hogwild_grid : c.nx;
+        const bool keep = (dbg & 1) != 0;
+        if (!c.hw.matches(samples, nnz) || c.hw.s != s_h || c.hw.balanced != (g_opt.balance != 0) ||
+            (keep && !c.hw.has_orig))
+            CHK(build_plan(c.hw, samples, nnz, s_h, g_opt.balance != 0, keep, st));
+        pl = &c.hw;
+    }
+    if (blocked && (dbg & 1) && !pl->has_orig)
+        return fail(MFSGD_ESTATE, "visit counting needs a plan made with debug bit 0 set");
 
     EpochLaunch a{};
     a.KP = c.KP;
@@ -404,15 +619,13 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
     a.lq = lq;
     a.spin_limit = (uint32_t)g_opt.spin_limit;
     a.err = c.err;
-    int rc;
     if (dbg & 1) {
-        if ((rc = grow(&c.visits, &c.visits_cap, nnz, "visit counters")))
-            return rc;
+        CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
         c.visits_n = nnz;
         HIPCHK(hipMemsetAsync(c.visits, 0, sizeof(uint32_t) * (size_t)(nnz > 0 ? nnz : 1), st));
         a.visits = c.visits;
     }
-    if (!wavefront) {
+    if (!blocked) {
         const int64_t nbatch = (nnz + a.f - 1) / a.f;
         int64_t W = g_opt.workers;
         if (W == 0) {
@@ -421,14 +634,15 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
                 return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
             W = (int64_t)c.cus * per_cu;
         }
-        if (W > nbatch)
-            W = nbatch;
+        W = std::min(W, nbatch);
         a.scheme = kSchemeHogwild;
         a.S = (const Sample*)samples;
         a.W = W;
+        a.sync_every = (int)g_opt.sync_every;
+        a.sync_l1 = (int)g_opt.sync_l1;
+        a.nx = c.nx;
         if (dbg & 2) {
-            if ((rc = grow(&c.trace, &c.trace_cap, nbatch, "trace")))
-                return rc;
+            CHK(grow(&c.trace, &c.trace_cap, nbatch, "trace"));
             c.trace_n = nbatch;
             HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)(nbatch > 0 ? nbatch : 1), st));
             a.trace_batch = c.trace;
@@ -440,24 +654,31 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
                 HIPCHK(epoch_f32(a, st));
         }
     } else {
-        const int s = c.plan_s;
+        const int s = pl->s;
+        int64_t want;
+        if (scheme == MFSGD_WAVEFRONT_DET)
+            want = 1;
+        else if (hog)
+            want = g_opt.workers > 0 ? std::max<int64_t>(1, g_opt.workers / s) : 0;
+        else
+            want = g_opt.team_waves;
         a.scheme = kSchemeWavefront;
-        a.S = c.Sp;
-        a.bstart = c.bstart;
+        a.S = pl->Sp;
+        a.bstart = pl->bstart;
         a.s = s;
-        a.team_waves = scheme == MFSGD_WAVEFRONT_DET ? 1 : (int)g_opt.waves_per_block;
+        CHK(team_layout(s, want, a));
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;
-        a.orig = (dbg & 1) ? c.orig : nullptr;
+        a.done = c.done;
+        a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
-            if ((rc = grow(&c.trace, &c.trace_cap, (int64_t)s * s, "trace")))
-                return rc;
+            CHK(grow(&c.trace, &c.trace_cap, (int64_t)s * s, "trace"));
             c.trace_n = (int64_t)s * s;
             HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)s * s, st));
             a.trace_wave = c.trace;
         }
-        HIPCHK(reset_tickets(c.tickets, s, c.err, st));
+        HIPCHK(reset_tickets(c.tickets, c.done, st));
         if (c.dtype == MFSGD_FP16)
             HIPCHK(epoch_f16(a, st));
         else
@@ -561,7 +782,8 @@ int mfsgd_plan(const mfsgd_sample* samples, int64_t nnz, int32_t s, void* stream
 int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q, int32_t scheme,
                 void* stream)
 {
-    return guarded([&]() -> int { return epoch_impl(samples, nnz, lr, lambda_p, lambda_q, scheme, (hipStream_t)stream); });
+    return guarded(
+        [&]() -> int { return epoch_impl(samples, nnz, lr, lambda_p, lambda_q, scheme, (hipStream_t)stream); });
 }
 
 int mfsgd_rmse(const mfsgd_sample* test, int64_t ntest, double* rmse_out, void* stream)
@@ -624,6 +846,6 @@ int mfsgd_finalize(void)
 
 const char* mfsgd_last_error(void) { return g_err.c_str(); }
 
-const char* mfsgd_version(void) { return "mfsgd 0.1 (gfx950)"; }
+const char* mfsgd_version(void) { return "mfsgd 0.2 (gfx950)"; }
 
 } // extern "C"

@@ -55,16 +55,34 @@ hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int
     return hipGetLastError();
 }
 
-__global__ void k_reset_tickets(uint32_t* t, int s)
+__global__ void k_reset_tickets(uint32_t* tickets, uint32_t* done)
 {
-    if ((int)threadIdx.x < s)
-        t[threadIdx.x] = 0u;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < kMaxGrid)
+        tickets[i] = 0u;
+    if (i < kMaxGrid * kMaxGrid)
+        done[i] = 0u;
 }
 
-hipError_t reset_tickets(uint32_t* t, int s, int* err, hipStream_t st)
+hipError_t reset_tickets(uint32_t* tickets, uint32_t* done, hipStream_t st)
 {
-    (void)err;
-    hipLaunchKernelGGL(k_reset_tickets, dim3(1), dim3(kMaxGrid), 0, st, t, s);
+    hipLaunchKernelGGL(k_reset_tickets, dim3(kMaxGrid * kMaxGrid / 256), dim3(256), 0, st, tickets, done);
+    return hipGetLastError();
+}
+
+// Which XCD (accelerator complex die) runs each workgroup: the hardware
+// register XCC_ID of gfx94x/gfx950.
+__global__ void k_probe_xcc(int* out)
+{
+    unsigned xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    if (threadIdx.x == 0)
+        out[blockIdx.x] = (int)(xcc & 0xf);
+}
+
+hipError_t probe_xcc(int* out, int n, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_probe_xcc, dim3(n), dim3(64), 0, st, out);
     return hipGetLastError();
 }
 
@@ -80,20 +98,89 @@ hipError_t reset_tickets(uint32_t* t, int s, int* err, hipStream_t st)
 // Chunks, steps and lanes are all taken in array order, so every block keeps
 // its samples in array order.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int block_of(int u, int v, int64_t m, int64_t n, int s)
+// Block cut: equal index ranges (floor(i*s/N)) when no bounds are given,
+// else the consecutive ranges bounds[0..s] (index i is in the last range
+// whose first index is <= i).
+struct Cut {
+    int64_t rb[kMaxGrid + 1];
+    int64_t cb[kMaxGrid + 1];
+    bool bounded;
+};
+
+__device__ __forceinline__ void load_cut(Cut& c, const int64_t* rbnd, const int64_t* cbnd, int s)
 {
+    c.bounded = rbnd != nullptr;
+    if (c.bounded)
+        for (int i = threadIdx.x; i <= s; i += blockDim.x) {
+            c.rb[i] = rbnd[i];
+            c.cb[i] = cbnd[i];
+        }
+}
+
+__device__ __forceinline__ int range_of(int64_t i, const int64_t* b, int s)
+{
+    int lo = 0, hi = s - 1; // largest k in [0, s-1] with b[k] <= i
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (b[mid] <= i)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int block_of(int u, int v, int64_t m, int64_t n, int s, const Cut& c)
+{
+    if (c.bounded)
+        return range_of(u, c.rb, s) * s + range_of(v, c.cb, s);
     const int rb = (int)(((int64_t)u * s) / m);
     const int cb = (int)(((int64_t)v * s) / n);
     return rb * s + cb;
 }
 
+// Per-index sample counts (users and items) for the balanced cut; indices out
+// of range are skipped and flagged.
+__global__ void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n, uint32_t* __restrict__ du,
+                          uint32_t* __restrict__ dv, int* bad)
+{
+    int found = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * blockDim.x) {
+        const int u = __builtin_nontemporal_load(&S[i].u);
+        const int v = __builtin_nontemporal_load(&S[i].v);
+        if (u < 0 || u >= m || v < 0 || v >= n) {
+            found = 1;
+            continue;
+        }
+        atomicAdd(du + u, 1u);
+        atomicAdd(dv + v, 1u);
+    }
+    if (found)
+        atomicOr(bad, 1);
+}
+
+hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, uint32_t* du, uint32_t* dv, int* bad,
+                        hipStream_t st)
+{
+    if (nnz <= 0)
+        return hipSuccess;
+    int64_t blocks = (nnz + 255) / 256;
+    if (blocks > 8192)
+        blocks = 8192;
+    hipLaunchKernelGGL(k_degrees, dim3((unsigned)blocks), dim3(256), 0, st, S, nnz, m, n, du, dv, bad);
+    return hipGetLastError();
+}
+
 __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
-                                                   int s, int32_t* __restrict__ counts, int* bad)
+                                                   int s, const int64_t* rbnd, const int64_t* cbnd,
+                                                   int32_t* __restrict__ counts, int* bad)
 {
     __shared__ int hist[kMaxGrid * kMaxGrid];
+    __shared__ Cut cut;
     const int nb = s * s;
     for (int i = threadIdx.x; i < nb; i += 64)
         hist[i] = 0;
+    load_cut(cut, rbnd, cbnd, s);
     __syncthreads();
     const int64_t cs = (nnz + kPlanChunks - 1) / kPlanChunks;
     const int64_t lo = (int64_t)blockIdx.x * cs;
@@ -106,7 +193,7 @@ __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S,
             found = 1;
             continue;
         }
-        atomicAdd(&hist[block_of(u, v, m, n, s)], 1);
+        atomicAdd(&hist[block_of(u, v, m, n, s, cut)], 1);
     }
     if (found)
         atomicOr(bad, 1);
@@ -182,14 +269,17 @@ __global__ __launch_bounds__(1024) void k_plan_scan_blocks(const int64_t* __rest
 }
 
 __global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
-                                                     int s, const int32_t* __restrict__ counts,
+                                                     int s, const int64_t* rbnd, const int64_t* cbnd,
+                                                     const int32_t* __restrict__ counts,
                                                      const int64_t* __restrict__ bstart, Sample* __restrict__ Sp,
                                                      int64_t* __restrict__ orig)
 {
     __shared__ int64_t base[kMaxGrid * kMaxGrid];
+    __shared__ Cut cut;
     const int nb = s * s;
     for (int b = threadIdx.x; b < nb; b += 64)
         base[b] = bstart[b] + counts[(int64_t)b * kPlanChunks + blockIdx.x];
+    load_cut(cut, rbnd, cbnd, s);
     __syncthreads();
     const int lane = threadIdx.x;
     const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
@@ -207,7 +297,7 @@ __global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ 
             x.r = __builtin_nontemporal_load(&S[i].r);
             valid = x.u >= 0 && x.u < m && x.v >= 0 && x.v < n; // the host never scatters a plan with bad indices
             if (valid)
-                b = block_of(x.u, x.v, m, n, s);
+                b = block_of(x.u, x.v, m, n, s, cut);
         }
         uint64_t pending = __ballot(valid);
         int64_t dest = -1;
@@ -236,7 +326,8 @@ hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s,
                       hipStream_t st)
 {
     const int nb = s * s;
-    hipLaunchKernelGGL(k_plan_count, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.counts, b.bad);
+    hipLaunchKernelGGL(k_plan_count, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd, b.counts,
+                       b.bad);
     hipLaunchKernelGGL(k_plan_scan_chunks, dim3(nb), dim3(256), 0, st, b.counts, b.totals);
     hipLaunchKernelGGL(k_plan_scan_blocks, dim3(1), dim3(1024), 0, st, b.totals, nb, b.bstart);
     return hipGetLastError();
@@ -245,8 +336,8 @@ hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s,
 hipError_t plan_scatter(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
                         hipStream_t st)
 {
-    hipLaunchKernelGGL(k_plan_scatter, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.counts, b.bstart, b.Sp,
-                       b.orig);
+    hipLaunchKernelGGL(k_plan_scatter, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd,
+                       b.counts, b.bstart, b.Sp, b.orig);
     return hipGetLastError();
 }
 

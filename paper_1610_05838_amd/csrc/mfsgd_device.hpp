@@ -51,12 +51,14 @@ struct Geo {
     static constexpr int A = KP / E;                 // lanes that hold values (32 or 64)
 };
 
+// Loads and stores of one lane's E values of a feature row.
 template <typename T, int E>
 struct Row {
     typedef typename VecT<T, E>::type V;
-    __device__ __forceinline__ static void load(const T* p, float (&x)[E])
+    __device__ __forceinline__ static V ld(const T* p) { return *reinterpret_cast<const V*>(p); }
+    __device__ __forceinline__ static void st(T* p, V v) { *reinterpret_cast<V*>(p) = v; }
+    __device__ __forceinline__ static void widen(V v, float (&x)[E])
     {
-        V v = *reinterpret_cast<const V*>(p);
         if constexpr (E == 1) {
             x[0] = (float)v;
         } else {
@@ -65,7 +67,7 @@ struct Row {
                 x[e] = (float)v[e];
         }
     }
-    __device__ __forceinline__ static void store(T* p, const float (&x)[E])
+    __device__ __forceinline__ static V narrow(const float (&x)[E])
     {
         V v;
         if constexpr (E == 1) {
@@ -75,8 +77,10 @@ struct Row {
             for (int e = 0; e < E; ++e)
                 v[e] = (T)x[e];
         }
-        *reinterpret_cast<V*>(p) = v;
+        return v;
     }
+    __device__ __forceinline__ static void load(const T* p, float (&x)[E]) { widen(ld(p), x); }
+    __device__ __forceinline__ static void store(T* p, const float (&x)[E]) { st(p, narrow(x)); }
 };
 
 // ---------------------------------------------------------------------------
@@ -207,6 +211,17 @@ __device__ __forceinline__ half_t from_f64<half_t>(double x)
     return __builtin_bit_cast(half_t, h);
 }
 
+// Cross-XCD coherence of the one-address-space batch-Hogwild!: every `every`
+// batches the XCD's leader wavefront writes its L2 back and invalidates it
+// (an agent-scope release + acquire), which bounds how long an update made on
+// one XCD stays invisible to the others; with `l1` the other wavefronts drop
+// their CU's L1 at the same points.
+struct CacheSync {
+    int every;   // batches between flushes, 0 = never
+    bool leader; // this wavefront flushes its XCD's L2
+    bool l1;     // this wavefront invalidates its CU's L1
+};
+
 // Debug hooks of one epoch.
 struct DebugSink {
     uint32_t* visits;     // per caller-array sample, or nullptr
@@ -230,20 +245,28 @@ struct DebugSink {
 // the end loads row 0 and is never used), so the compiler can keep all D
 // samples' loads in flight with counted waits.
 // ---------------------------------------------------------------------------
+// by-value select (keeps the operands in registers)
+template <typename V>
+__device__ __forceinline__ V pick(bool c, V a, V b)
+{
+    return c ? a : b;
+}
+
 template <int KP, typename T, int D>
 struct WorkerState {
     static constexpr int E = Geo<KP>::E;
-    float sp[D][E], sq[D][E]; // rows in flight
+    typedef typename VecT<T, E>::type V;
+    V sp[D], sq[D]; // rows in flight, as loaded
     int su[D], sv[D];
     float sr[D];
-    float hp[D][E], hq[D][E]; // new rows of the last D samples
+    V hp[D], hq[D]; // rows of the last D samples, as stored
     int hu[D], hv[D];
 };
 
 template <int KP, typename T, int D, bool DBG>
 __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t worker,
                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
-                                           float lq, const DebugSink dbg)
+                                           float lq, const DebugSink dbg, const CacheSync sync = CacheSync{0, false, false})
 {
     constexpr int E = Geo<KP>::E;
     constexpr int A = Geo<KP>::A;
@@ -284,13 +307,12 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
     load_chunk(n_batch, n_off, nU, nV, nR, ncnt);
 
     WorkerState<KP, T, D> st;
+    typedef typename WorkerState<KP, T, D>::V V;
 #pragma unroll
     for (int d = 0; d < D; ++d) {
         st.su[d] = st.sv[d] = st.hu[d] = st.hv[d] = -1;
         st.sr[d] = 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            st.sp[d][e] = st.sq[d][e] = st.hp[d][e] = st.hq[d][e] = 0.f;
+        st.sp[d] = st.sq[d] = st.hp[d] = st.hq[d] = V{};
     }
 
     // request the rows of the sample at lane `xl` of a chunk's metadata
@@ -302,33 +324,31 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         st.su[slot] = ok ? u : -1;
         st.sv[slot] = ok ? v : -1;
         st.sr[slot] = r;
-        R::load(P + (int64_t)(ok ? u : 0) * KP + col, st.sp[slot]);
-        R::load(Q + (int64_t)(ok ? v : 0) * KP + col, st.sq[slot]);
+        st.sp[slot] = R::ld(P + (int64_t)(ok ? u : 0) * KP + col);
+        st.sq[slot] = R::ld(Q + (int64_t)(ok ? v : 0) * KP + col);
     };
 
     // update the sample in slot j
     auto process = [&](int j, int64_t pos) {
-        float p[E], q[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            p[e] = st.sp[j][e];
-            q[e] = st.sq[j][e];
-        }
         const int u = st.su[j], v = st.sv[j];
+        // a row that one of the previous D-1 samples rewrote is taken from that
+        // sample's stored value (whole vectors; the nearest writer wins)
+        V pv = st.sp[j], qv = st.sq[j];
 #pragma unroll
         for (int d = D - 1; d >= 1; --d) {
             const int h = (j - d + D) % D;
-            const bool fu = st.hu[h] == u, fv = st.hv[h] == v;
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                p[e] = fu ? st.hp[h][e] : p[e];
-                q[e] = fv ? st.hq[h][e] : q[e];
-            }
+            pv = pick(st.hu[h] == u, st.hp[h], pv);
+            qv = pick(st.hv[h] == v, st.hq[h], qv);
         }
+        float p[E], q[E];
+        R::widen(pv, p);
+        R::widen(qv, q);
         float dot = 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e)
             dot += p[e] * q[e];
+        if constexpr (A < 64)
+            dot = holds ? dot : 0.f; // idle lanes hold a copy of column 0
         dot = wave_sum(dot);
         const float err = st.sr[j] - dot;
 #pragma unroll
@@ -337,17 +357,15 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
             p[e] = pe + lr * (err * qe - lp * pe);
             q[e] = qe + lr * (err * pe - lq * qe);
         }
+        const V np = R::narrow(p), nq = R::narrow(q);
         if (holds) {
-            R::store(P + (int64_t)u * KP + col, p);
-            R::store(Q + (int64_t)v * KP + col, q);
+            R::st(P + (int64_t)u * KP + col, np);
+            R::st(Q + (int64_t)v * KP + col, nq);
         }
         st.hu[j] = u;
         st.hv[j] = v;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            st.hp[j][e] = p[e];
-            st.hq[j][e] = q[e];
-        }
+        st.hp[j] = np;
+        st.hq[j] = nq;
         if constexpr (DBG) {
             if (dbg.visits && lane == 0) {
                 const int64_t idx = dbg.orig ? dbg.orig[pos] : pos;
@@ -356,6 +374,7 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         }
     };
 
+    int batches = 0;
     // prologue: positions 0 .. D-2 of the first chunk
 #pragma unroll
     for (int d = 0; d < D - 1; ++d)
@@ -369,6 +388,14 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         if constexpr (DBG) {
             if (dbg.trace && c_off == 0 && lane == 0)
                 dbg.trace[c_batch] = (int32_t)worker;
+        }
+        if (sync.every > 0 && c_off == 0 && ++batches % sync.every == 0) {
+            if (sync.leader) {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            } else if (sync.l1) {
+                asm volatile("buffer_inv sc0" ::: "memory");
+            }
         }
         for (int g = 0; g < 64 - D; g += D) { // look-ahead stays inside this chunk
 #pragma unroll

@@ -9,39 +9,66 @@ namespace mfsgd {
 
 constexpr int kHogwildBlock = 256; // 4 wavefronts per workgroup, each an independent worker
 
-// batch-Hogwild! epoch (section 3.2.2): wavefront w of the grid is worker w.
+// batch-Hogwild! over the whole GPU in one address space (section 3.2.2):
+// wavefront w of the grid is worker w.  The XCDs' L2 caches are not coherent
+// with each other, so rows that several XCDs touch are updated in per-XCD
+// copies until evicted; the block-scheduled kernel below is the coherent form.
 template <int KP, typename T, int D, bool DBG>
 __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restrict__ S, int64_t nnz, int64_t W,
                                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr,
-                                                           float lp, float lq, DebugSink dbg)
+                                                           float lp, float lq, DebugSink dbg, int sync_every,
+                                                           int sync_l1, int nx)
 {
     const int64_t worker = uniform64((int64_t)blockIdx.x * (kHogwildBlock / 64) + (threadIdx.x >> 6));
     if (worker >= W)
         return;
-    run_worker<KP, T, D, DBG>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg);
+    // workgroups are dealt to XCDs round-robin: the first wavefront of each of
+    // the first nx workgroups leads its XCD's cache flushes
+    const CacheSync sync{sync_every, (int)blockIdx.x < nx && (threadIdx.x >> 6) == 0, sync_l1 != 0};
+    run_worker<KP, T, D, DBG>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
 }
 
-// Wavefront-update epoch (section 3.2.3).  Workgroup i is worker i (a team of
-// blockDim/64 wavefronts) and owns row block i.  In wave w it takes column
-// block sigma_i(w) = C[(i + O[w]) mod s] once that column's ticket reads w,
-// runs batch-Hogwild! over the block with its wavefronts, and releases the
-// column by storing w+1.  Every column is used by exactly one worker per
-// wave, so the ticket of a column counts the waves completed on it.
-// Release/acquire at agent scope make one team's feature writes visible to
-// the next team that takes the column, whichever XCD either runs on.  A wait
-// that exceeds spin_limit polls raises *err and every team leaves.
+// Block-scheduled epoch: wavefront-update (section 3.2.3), and
+// batch-Hogwild! partitioned over the GPU's coherence domains.
+//
+// The s x s grid of blocks is processed in s waves.  Worker (team) i owns row
+// block i and in wave w takes column block sigma_i(w) = C[(i + O[w]) mod s],
+// so the blocks of one wave share no row and no column.  Column tickets order
+// the waves: team i starts wave w once ticket[sigma_i(w)] reads w, and the
+// last member to finish releases it with w+1 (every column is used by exactly
+// one team per wave, so a ticket counts the waves completed on its column).
+//
+// A team is G workgroups; inside a block its G*blockDim/64 wavefronts run
+// batch-Hogwild! (run_worker) over the block's samples.  Members do not wait
+// for each other between waves (they share the team's row block, which no
+// other team touches); the last one to finish a wave releases its column.  Team placement
+// follows the hardware: workgroup b runs on XCD b mod nx (round-robin
+// dispatch, checked at init), and every member of a team sits on one XCD, so
+// the team's unsynchronised updates meet in that XCD's shared L2.  Feature
+// rows move between teams only at block hand-over, through an agent-scope
+// release (L2 write-back) and acquire (L1/L2 invalidate), whichever XCDs the
+// two teams run on.  With nx = 1 the layout is placement-agnostic (used for
+// one-wavefront teams).
+//
+// A ticket wait that exceeds spin_limit polls raises *err; every waiting
+// workgroup then leaves, so the grid always drains.
 template <int KP, typename T, int D, bool DBG>
-__global__ __launch_bounds__(1024) void k_wavefront(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
-                                                    int s, uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
-                                                    T* __restrict__ Q, float lr, float lp, float lq, int f,
-                                                    uint32_t* tickets, uint32_t spin_limit, int* err, DebugSink dbg,
-                                                    int32_t* trace)
+__global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
+                                                  int s, int nx, int tpx, int G, uint64_t sigma_c, uint64_t sigma_o,
+                                                  T* __restrict__ P, T* __restrict__ Q, float lr, float lp, float lq,
+                                                  int f, uint32_t* tickets, uint32_t* done, uint32_t spin_limit,
+                                                  int* err, DebugSink dbg, int32_t* trace)
 {
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
     __shared__ int abort_all;
-    const int team = blockIdx.x;
+    const int xcc = (int)(blockIdx.x % (unsigned)nx);
+    const int idx = (int)(blockIdx.x / (unsigned)nx);
+    const int team = (idx % tpx) * nx + xcc;
+    const int member = idx / tpx;
     const int waves = blockDim.x >> 6;
     const int wv = uniform(threadIdx.x >> 6);
+    const int64_t W = (int64_t)G * waves;
+    const int64_t worker = (int64_t)member * waves + wv;
     if (threadIdx.x == 0) {
         shuffle_perm(sigma_c, s, Cperm);
         shuffle_perm(sigma_o, s, Ooff);
@@ -53,34 +80,72 @@ __global__ __launch_bounds__(1024) void k_wavefront(const Sample* __restrict__ S
     for (int w = 0; w < s; ++w) {
         const int col = Cperm[(team + Ooff[w]) % s];
         if (threadIdx.x == 0) {
+            // Poll with an atomic read-modify-write: it is resolved at the
+            // device's coherence point, whereas a plain (even agent-scope) load
+            // may keep hitting a stale copy in this XCD's L2.  Acquire once the
+            // ticket has come round, which invalidates this CU's L1 and this
+            // XCD's L2 before the block's rows are read.
             uint32_t polls = 0;
-            while (__hip_atomic_load(tickets + col, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != (uint32_t)w) {
-                if (++polls > spin_limit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                    __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            while (__hip_atomic_fetch_or(tickets + col, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) !=
+                   (uint32_t)w) {
+                if (++polls > spin_limit ||
+                    __hip_atomic_fetch_or(err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                    __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     abort_all = 1;
                     break;
                 }
                 __builtin_amdgcn_s_sleep(4);
             }
-            if (trace)
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            if (trace && member == 0)
                 trace[(int64_t)team * s + w] = col;
         }
         __syncthreads();
         if (abort_all)
             return;
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const int64_t b = (int64_t)team * s + col;
         const int64_t lo = bstart[b], hi = bstart[b + 1];
         if (hi > lo) {
             DebugSink blk = inner;
             if (blk.orig)
                 blk.orig += lo;
-            run_worker<KP, T, D, DBG>(Sp + lo, hi - lo, waves, wv, f, P, Q, lr, lp, lq, blk);
+            run_worker<KP, T, D, DBG>(Sp + lo, hi - lo, W, worker, f, P, Q, lr, lp, lq, blk);
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        __syncthreads();
-        if (threadIdx.x == 0)
-            __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads(); // every wavefront of this workgroup is done with the block
+        if (threadIdx.x == 0) {
+            if (G == 1) {
+                __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                // one counter per (team, wave): a member may already be in the
+                // next wave (its next column can come free first) while another
+                // is still finishing this one
+                const uint32_t before = __hip_atomic_fetch_add(done + (int64_t)team * s + w, 1u, __ATOMIC_ACQ_REL,
+                                                               __HIP_MEMORY_SCOPE_AGENT);
+                if (before == (uint32_t)(G - 1)) // last member of the team to finish this wave
+                    __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+}
+
+template <int KP, typename T, int D>
+static int occupancy_blocked_t(int threads)
+{
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false>, threads, 0) != hipSuccess)
+        return 0;
+    return blocks;
+}
+
+template <int KP, typename T>
+static int occupancy_blocked_kp(int depth, int threads)
+{
+    switch (depth) {
+    case 1: return occupancy_blocked_t<KP, T, 1>(threads);
+    case 2: return occupancy_blocked_t<KP, T, 2>(threads);
+    case 4: return occupancy_blocked_t<KP, T, 4>(threads);
+    case 8: return occupancy_blocked_t<KP, T, 8>(threads);
+    default: return 0;
     }
 }
 
@@ -157,12 +222,13 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         const int64_t blocks = (a.W + 3) / 4;
         const DebugSink dbg{a.visits, nullptr, a.trace_batch};
         hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st, a.S,
-                           a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg);
+                           a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
-        hipLaunchKernelGGL((k_wavefront<KP, T, D, DBG>), dim3((unsigned)a.s), dim3(64 * a.team_waves), 0, st, a.S,
-                           a.bstart, a.s, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets,
-                           a.spin_limit, a.err, dbg, a.trace_wave);
+        const unsigned grid = (unsigned)(a.s * a.wg_per_team);
+        hipLaunchKernelGGL((k_blocked<KP, T, D, DBG>), dim3(grid), dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s,
+                           a.nx, a.s / a.nx, a.wg_per_team, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f,
+                           a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave);
     }
     return hipGetLastError();
 }
@@ -245,6 +311,17 @@ struct Dispatch {
         case 128: return occupancy_kp<128, T>(depth);
         case 256: return occupancy_kp<256, T>(depth);
         case 512: return occupancy_kp<512, T>(depth);
+        default: return 0;
+        }
+    }
+    static int occupancy_blocked(int KP, int depth, int threads)
+    {
+        switch (KP) {
+        case 32: return occupancy_blocked_kp<32, T>(depth, threads);
+        case 64: return occupancy_blocked_kp<64, T>(depth, threads);
+        case 128: return occupancy_blocked_kp<128, T>(depth, threads);
+        case 256: return occupancy_blocked_kp<256, T>(depth, threads);
+        case 512: return occupancy_blocked_kp<512, T>(depth, threads);
         default: return 0;
         }
     }

@@ -7,6 +7,11 @@ hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st) { return Dispatch<hal
 
 int occupancy_f16(int KP, int depth) { return Dispatch<half_t>::occupancy(KP, depth); }
 
+int occupancy_blocked_f16(int KP, int depth, int threads)
+{
+    return Dispatch<half_t>::occupancy_blocked(KP, depth, threads);
+}
+
 hipError_t rmse_partial_f16(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
                            hipStream_t st)
 {

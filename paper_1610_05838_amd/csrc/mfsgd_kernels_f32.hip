@@ -7,6 +7,11 @@ hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st) { return Dispatch<flo
 
 int occupancy_f32(int KP, int depth) { return Dispatch<float>::occupancy(KP, depth); }
 
+int occupancy_blocked_f32(int KP, int depth, int threads)
+{
+    return Dispatch<float>::occupancy_blocked(KP, depth, threads);
+}
+
 hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
                            hipStream_t st)
 {

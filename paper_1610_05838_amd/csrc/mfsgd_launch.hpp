@@ -27,12 +27,17 @@ struct EpochLaunch {
     void* P;
     void* Q;
     float lr, lp, lq;
-    // wavefront-update
+    int sync_every;  // one-address-space batch-Hogwild!: batches between XCD cache flushes (0 = none)
+    int sync_l1;     // ... and whether the other wavefronts drop their CU's L1 then
+    // block-scheduled epochs
     const int64_t* bstart;
-    int s;
-    int team_waves;
+    int s;           // grid side
+    int nx;          // coherence domains (XCDs) the teams are spread over; s % nx == 0
+    int wg_per_team; // workgroups per team
+    int wg_waves;    // wavefronts per workgroup
     uint64_t sigma_c, sigma_o;
     uint32_t* tickets;
+    uint32_t* done;  // arrival counters, one per (team, wave): s*s entries
     uint32_t spin_limit;
     int* err;
     int32_t* trace_wave;
@@ -47,6 +52,8 @@ hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st);
 hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st);
 int occupancy_f32(int KP, int depth);
 int occupancy_f16(int KP, int depth);
+int occupancy_blocked_f32(int KP, int depth, int threads); // workgroups per CU
+int occupancy_blocked_f16(int KP, int depth, int threads);
 hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
                             hipStream_t st);
 hipError_t rmse_partial_f16(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
@@ -57,16 +64,24 @@ hipError_t init_f16(void* A, int64_t rows, int k, int KP, uint64_t stream, doubl
 // Implemented in mfsgd_aux.hip (type-independent kernels).
 hipError_t rmse_final(const double* partial, int64_t ntest, double* out, hipStream_t st);
 hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int* bad, hipStream_t st);
-hipError_t reset_tickets(uint32_t* t, int s, int* err, hipStream_t st);
+// zero the column tickets and the kMaxGrid^2 arrival counters (a fill kernel, safe under graph capture)
+hipError_t reset_tickets(uint32_t* tickets, uint32_t* done, hipStream_t st);
+// XCC id of each of `n` one-wavefront workgroups (to learn the dispatch layout)
+hipError_t probe_xcc(int* out, int n, hipStream_t st);
 // stable bucketing of samples into the s x s grid
 struct PlanBuffers {
-    int32_t* counts;   // s*s*chunks, bin-major
-    int64_t* totals;   // s*s
-    int64_t* bstart;   // s*s+1
-    Sample* Sp;        // planned copy
-    int64_t* orig;     // planned position -> caller position (optional)
-    int* bad;          // index-range flag
+    int32_t* counts;     // s*s*chunks, bin-major
+    int64_t* totals;     // s*s
+    int64_t* bstart;     // s*s+1
+    Sample* Sp;          // planned copy
+    int64_t* orig;       // planned position -> caller position (optional)
+    int* bad;            // index-range flag
+    const int64_t* rbnd; // balanced cut (s+1 user bounds), or nullptr for equal ranges
+    const int64_t* cbnd; // s+1 item bounds
 };
+// per-index sample counts for the balanced cut (indices out of range raise *bad)
+hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, uint32_t* du, uint32_t* dv, int* bad,
+                        hipStream_t st);
 constexpr int kPlanChunks = 2048;
 // counts, per-block scans and block starts; raises *b.bad on an index out of range
 hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,

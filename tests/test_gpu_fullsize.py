@@ -1,0 +1,82 @@
+"""Full-size checks on the Netflix-shaped workload the benchmark times
+(m=480,189, n=17,770, k=128, 99,072,112 training and 1,408,395 test ratings,
+binary32).  The serial oracle needs minutes per epoch at this size, so these
+are properties that hold at any size plus outputs the oracle computes one by
+one (the test RMSE of the trained factors)."""
+import numpy as np
+import pytest
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def M():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1610_05838_amd import mfsgd
+    mfsgd.lib()
+    yield mfsgd
+    mfsgd.finalize()
+
+
+@pytest.fixture(scope="module")
+def netflix(M, gen):
+    w = gen.workload("netflix")
+    S, T = gen.make(w)
+    return w, S, T, M.samples_to_device(S), M.samples_to_device(T)
+
+
+def reset(M, **opts):
+    o = dict(dtype=0, batch_f=256, workers=0, depth=4, team_waves=0, partition=2, hogwild_grid=0, balance=1,
+             sync_every=0, sync_l1=0, spin_limit=1 << 24, debug=0)
+    o.update(opts)
+    for k, v in o.items():
+        M.set_option(k, v)
+
+
+def test_bench_configuration_visits_every_sample_and_trains(M, netflix):
+    import torch
+    w, S, T, dS, dT = netflix
+    reset(M, debug=1)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    assert M.get_option("partitioned") == 0  # 255 MB of factors: one address space
+    r0 = M.rmse(dT)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    v = M.debug_visits(len(S))
+    assert bool(torch.all(v == 1)), "a sample was skipped or used twice"
+    M.set_option("debug", 0)
+    hist = [r0, M.rmse(dT)]
+    for t in range(1, 3):
+        M.epoch(dS, w["lr"] * w["decay"] ** t, w["lam"], w["lam"], "hogwild")
+        hist.append(M.rmse(dT))
+    print("test rmse by epoch", hist)
+    assert all(b < a for a, b in zip(hist, hist[1:]))
+    assert hist[-1] < 1.05  # the serial oracle reaches 0.939 after 3 epochs here
+
+
+def test_rmse_kernel_matches_oracle_on_trained_factors(M, netflix):
+    w, S, T, dS, dT = netflix
+    reset(M)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    P, Q = M.get_factors(w["m"], w["n"], w["k"])
+    P, Q = P.cpu().numpy(), Q.cpu().numpy()
+    assert M.rmse(dT) == pytest.approx(oracle.rmse(P, Q, T), rel=1e-6)
+    sub = T[:: 97]
+    assert M.rmse(M.samples_to_device(sub)) == pytest.approx(float(np.sqrt(oracle.sq_errors(P, Q, sub).mean())),
+                                                             rel=1e-6)
+
+
+def test_partitioned_form_at_full_size(M, netflix):
+    import torch
+    w, S, T, dS, dT = netflix
+    reset(M, partition=1, debug=3)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    x = M.get_option("xcds")
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    assert bool(torch.all(M.debug_visits(len(S)) == 1))
+    tr = M.debug_trace(x * x).cpu().numpy().reshape(x, x)
+    assert np.array_equal(tr, oracle.wavefront_sigma(w["seed"], 0, x))

@@ -20,7 +20,8 @@ import oracle
 pytestmark = pytest.mark.gpu
 
 TOL = {np.float32: 1e-4, np.float16: 2e-2}
-DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=4, waves_per_block=8, spin_limit=1 << 24, debug=0)
+DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=4, team_waves=0, partition=2, hogwild_grid=0, balance=1,
+                sync_every=0, sync_l1=0, spin_limit=1 << 24, debug=0)
 
 
 @pytest.fixture(scope="module")
@@ -129,7 +130,7 @@ def test_single_worker_equals_serial(M, depth, dtype, k):
     for m, n, nnz in ((7, 5, 2000), (400, 300, 6001)):
         S = rand_samples(rng, m, n, nnz) if m > 7 else forwarding_stress(rng, nnz)
         seed = 77 + k
-        setup(M, m, n, k, seed, dtype, workers=1, depth=depth)
+        setup(M, m, n, k, seed, dtype, workers=1, depth=depth, partition=0)
         M.epoch(M.samples_to_device(S), 0.01, 0.05, 0.04, "hogwild")
         P, Q = factors(M, m, n, k, dtype)
         Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
@@ -140,7 +141,7 @@ def test_single_worker_equals_serial(M, depth, dtype, k):
 def test_tiny_workload_single_worker_equals_serial(M, gen):
     w = gen.workload("tiny")
     S, T = gen.make(w)
-    setup(M, w["m"], w["n"], w["k"], w["seed"], workers=1)
+    setup(M, w["m"], w["n"], w["k"], w["seed"], workers=1, partition=0)
     dS = M.samples_to_device(S)
     Po, Qo = oracle.init_factors(w["m"], w["n"], w["k"], w["seed"], np.float32)
     for t in range(2):
@@ -153,22 +154,54 @@ def test_tiny_workload_single_worker_equals_serial(M, gen):
 
 # ---------------------------------------------------------------------------- schedules, coverage
 def test_hogwild_schedule_and_coverage(M):
+    """One address space: batch b goes to worker b mod W and every sample is
+    used once; partitioned over the XCDs: every sample once and the blocks
+    follow the column orders of the oracle."""
     rng = np.random.default_rng(3)
-    m, n, nnz = 3000, 2000, 1_000_003  # ragged last batch
+    m, n, nnz, seed = 3000, 2000, 1_000_003, 9  # ragged last batch
     S = rand_samples(rng, m, n, nnz)
-    setup(M, m, n, 128, 9, debug=3)
-    W = 1000
-    M.set_option("workers", W)
-    M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
-    vis = M.debug_visits(nnz).cpu().numpy()
-    assert np.all(vis == 1)
-    nb = (nnz + 255) // 256
-    tr = M.debug_trace(nb).cpu().numpy()
-    assert np.array_equal(tr, oracle.hogwild_batch_owner(nnz, 256, W))
-    # auto worker count: still every sample exactly once
-    M.set_option("workers", 0)
-    M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
+    dS = M.samples_to_device(S)
+    setup(M, m, n, 128, seed, debug=3, partition=0, workers=1000)
+    M.epoch(dS, 0.001, 0.05, 0.05, "hogwild")
     assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+    nb = (nnz + 255) // 256
+    assert np.array_equal(M.debug_trace(nb).cpu().numpy(), oracle.hogwild_batch_owner(nnz, 256, 1000))
+    M.set_option("workers", 0)  # as many workers as stay resident
+    M.epoch(dS, 0.001, 0.05, 0.05, "hogwild")
+    assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+    M.set_option("partition", 1)
+    x = M.get_option("xcds")
+    for t in range(2, 4):
+        M.epoch(dS, 0.001, 0.05, 0.05, "hogwild")
+        assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+        tr = M.debug_trace(x * x).cpu().numpy().reshape(x, x)
+        assert np.array_equal(tr, oracle.wavefront_sigma(seed, t, x))
+
+
+def test_xcd_layout_detected(M):
+    setup(M, 10, 10, 8, 1)
+    x = M.get_option("xcds")
+    print(f"xcds={x} cus={M.get_option('cus')}")
+    assert x >= 1 and M.get_option("cus") % x == 0
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_partitioned_hogwild_single_wave_teams_match_oracle(M, gen, dtype):
+    """Partitioned batch-Hogwild! with one wavefront per team is the wavefront
+    schedule on the XCD grid with serial blocks: compare with the oracle."""
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, dtype, partition=1)
+    x = M.get_option("xcds")
+    M.set_option("workers", x)  # one wavefront per team
+    dS = M.samples_to_device(S)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(2):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+        oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], x, seed, t, balanced=True)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
 
 @pytest.mark.parametrize("scheme", ["wavefront", "wavefront_det"])
@@ -187,19 +220,20 @@ def test_wavefront_schedule_and_coverage(M, scheme):
 
 
 # ---------------------------------------------------------------------------- deterministic wavefront
+@pytest.mark.parametrize("balance", [0, 1])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 @pytest.mark.parametrize("s", [1, 3, 8, 32])
-def test_wavefront_det_matches_oracle(M, gen, dtype, s):
+def test_wavefront_det_matches_oracle(M, gen, dtype, s, balance):
     w = gen.workload("tiny")
     S, _ = gen.make(w)
     m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
-    setup(M, m, n, k, seed, dtype)
+    setup(M, m, n, k, seed, dtype, balance=balance)
     dS = M.samples_to_device(S)
     M.plan(dS, s)
     Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
     for t in range(2):
         M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
-        oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, t)
+        oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, t, balanced=bool(balance))
     P, Q = factors(M, m, n, k, dtype)
     assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
@@ -213,7 +247,7 @@ def test_wavefront_det_k128_zipf(M, gen):
     M.plan(dS, s)
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
     Po, Qo = oracle.init_factors(m, n, k, seed, np.float32)
-    oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0)
+    oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0, balanced=True)
     P, Q = factors(M, m, n, k, np.float32)
     assert maxabs(P, Po) <= 1e-4 and maxabs(Q, Qo) <= 1e-4
 
@@ -234,7 +268,7 @@ def test_checkpoint_resume_is_bitwise(M, gen):
     M.epoch(dS, 0.01, 0.05, 0.05, "wavefront_det")
     P1, Q1 = M.get_factors(m, n, k)
     t = M.get_epoch()
-    setup(M, m, n, k, 999)  # a different model, then restore
+    setup(M, m, n, k, seed)  # a fresh model with the same seed (the seed keys the column orders), then restore
     M.set_factors(P1, Q1)
     M.set_epoch(t)
     M.plan(dS, s)
@@ -262,20 +296,58 @@ def test_lr_zero_is_identity(M, scheme, dtype):
 
 
 # ---------------------------------------------------------------------------- Hogwild! convergence parity
+def scaled_tiny(gen, scale):
+    """The tiny workload's model and density on an (m, n) grid `scale` times larger
+    in each direction."""
+    w = gen.workload("tiny", m=1000 * scale, n=500 * scale, ntrain=49_500 * scale * scale,
+                     ntest=500 * scale * scale, seed=gen.SEED_BASE + 11)
+    return w, *gen.make(w)
+
+
+@pytest.mark.parametrize("partition", [2, 1])
 @pytest.mark.parametrize("dtype,tol", [(np.float32, 1e-3), (np.float16, 5e-3)])
-def test_hogwild_rmse_gap_tiny(M, gen, dtype, tol):
-    w = gen.workload("tiny")
-    S, T = gen.make(w)
+def test_hogwild_rmse_gap(M, gen, dtype, tol, partition):
+    """batch-Hogwild! with workers well below min(m, n) (the paper's condition for
+    Hogwild! to behave like serial SGD): the test RMSE after 5 epochs is within
+    tol of the serial oracle's.  Tiny-workload model on a 4000 x 2000 grid, 8
+    XCD teams of 4 wavefronts (the automatic choice partitions a model this
+    small)."""
+    w, S, T = scaled_tiny(gen, 4)
     m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
-    setup(M, m, n, k, seed, dtype)
+    setup(M, m, n, k, seed, dtype, partition=partition, workers=32)
+    assert M.get_option("partitioned") == 1
     dS, dT = M.samples_to_device(S), M.samples_to_device(T)
     Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
-    for t in range(w["epochs"]):
+    for t in range(5):
         M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
         oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
     got, want = M.rmse(dT), oracle.rmse(Po, Qo, T)
-    print(f"tiny hogwild rmse gpu={got:.6f} oracle={want:.6f}")
+    print(f"hogwild partition={partition} rmse gpu={got:.6f} oracle={want:.6f} gap={got - want:+.6f}")
     assert abs(got - want) <= tol
+
+
+def test_one_address_space_hogwild_on_a_small_model(M, gen):
+    """The one-address-space form on a model that fits in every XCD's L2: the
+    XCDs update their own cached copies, so the RMSE trails the serial oracle's
+    by more than the Hogwild! tolerance (measured about 8e-3 here); it still
+    trains.  This records the reason the automatic choice partitions small
+    models."""
+    w, S, T = scaled_tiny(gen, 4)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, partition=0, workers=32)
+    assert M.get_option("partitioned") == 0
+    dS, dT = M.samples_to_device(S), M.samples_to_device(T)
+    hist = [M.rmse(dT)]
+    for t in range(5):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+        hist.append(M.rmse(dT))
+    Po, Qo = oracle.init_factors(m, n, k, seed, np.float32)
+    for t in range(5):
+        oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
+    want = oracle.rmse(Po, Qo, T)
+    print(f"one address space rmse {hist} oracle {want:.6f}")
+    assert all(b < a for a, b in zip(hist, hist[1:]))
+    assert abs(hist[-1] - want) < 0.05
 
 
 # ---------------------------------------------------------------------------- errors

@@ -289,8 +289,8 @@ def test_block_order_is_stable_bucketing(orc):
             assert orc.row_block(S[i]["u"], m, s) * s + orc.col_block(S[i]["v"], n, s) == b
 
 
-def _wavefront_sequence(orc, S, m, n, s, seed, t, reverse_workers=False):
-    order, start = orc.block_order(S, m, n, s)
+def _wavefront_sequence(orc, S, m, n, s, seed, t, reverse_workers=False, balanced=False):
+    order, start = orc.block_order(S, m, n, s, balanced)
     sig = orc.wavefront_sigma(seed, t, s)
     seq = []
     for w in range(s):
@@ -301,8 +301,9 @@ def _wavefront_sequence(orc, S, m, n, s, seed, t, reverse_workers=False):
     return np.array(seq, dtype=np.int64)
 
 
+@pytest.mark.parametrize("balanced", [False, True])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-def test_wavefront_blocks_commute(orc, dtype):
+def test_wavefront_blocks_commute(orc, dtype, balanced):
     """Blocks of one wave share no row and no column (independent samples,
     section 2.3), so the wavefront epoch equals a serial epoch over its schedule
     with the workers of every wave taken in either order."""
@@ -311,9 +312,9 @@ def test_wavefront_blocks_commute(orc, dtype):
     S = samples([(rng.integers(m), rng.integers(n), rng.uniform(1, 5)) for _ in range(3000)], orc)
     P, Q = orc.init_factors(m, n, k, seed, dtype)
     Pw, Qw = P.copy(), Q.copy()
-    orc.epoch_wavefront(Pw, Qw, S, 0.02, 0.05, 0.05, s, seed, 3)
+    orc.epoch_wavefront(Pw, Qw, S, 0.02, 0.05, 0.05, s, seed, 3, balanced)
     for rev in (False, True):
-        seq = _wavefront_sequence(orc, S, m, n, s, seed, 3, rev)
+        seq = _wavefront_sequence(orc, S, m, n, s, seed, 3, rev, balanced)
         assert sorted(seq.tolist()) == list(range(len(S)))
         Ps, Qs = P.copy(), Q.copy()
         orc.epoch_serial(Ps, Qs, S[seq], 0.02, 0.05, 0.05)
@@ -359,3 +360,56 @@ def test_hogwild_single_worker_is_serial_order(orc):
     assert own.tolist() == [0, 0, 0, 0]
     own = orc.hogwild_batch_owner(1025, 256, 3)
     assert own.tolist() == [0, 1, 2, 0, 1]
+
+
+def _range_loads(counts, bounds):
+    return [int(sum(counts[bounds[k]:bounds[k + 1]])) for k in range(len(bounds) - 1)]
+
+
+def test_balanced_bounds_are_optimal(orc):
+    """Brute force over every way of cutting a short index range into s consecutive
+    (possibly empty) ranges: the oracle's cut reaches the smallest possible
+    largest-range load, its ranges cover 0..N in order, and each index lands in
+    its range."""
+    rng = np.random.default_rng(21)
+    for trial in range(40):
+        N = int(rng.integers(1, 9))
+        s = int(rng.integers(1, 5))
+        nnz = int(rng.integers(0, 40))
+        u = np.minimum(rng.zipf(1.5, nnz) - 1, N - 1) if nnz else np.zeros(0, int)
+        S = samples([(int(x), 0, 1.0) for x in u], orc)
+        counts = np.bincount(S["u"], minlength=N) if nnz else np.zeros(N, int)
+        b = orc.balanced_bounds(S, N, 0, s).tolist()
+        assert b[0] == 0 and b[-1] == N and all(x <= y for x, y in zip(b, b[1:]))
+        best = min(max(_range_loads(counts, [0, *cuts, N]))
+                   for cuts in itertools.combinations_with_replacement(range(N + 1), s - 1))
+        assert max(_range_loads(counts, b)) == best
+        for i in range(N):
+            k = orc.bounded_block(i, b, s)
+            assert b[k] <= i < b[k + 1]
+
+
+def test_balanced_blocks_even_out_skew(orc, gen):
+    """Netflix-shaped skew: equal index ranges leave a block row 1.5x heavier than
+    the mean; the optimal contiguous cut brings it close to the mean."""
+    w = gen.workload("netflix", ntrain=400_000, ntest=0)
+    S = gen.draw(w, 0, w["ntrain"])
+    s = 8
+    for which, N, col in ((0, w["m"], "u"), (1, w["n"], "v")):
+        counts = np.bincount(S[col], minlength=N)
+        b = orc.balanced_bounds(S, N, which, s)
+        loads = _range_loads(counts, b)
+        assert sum(loads) == len(S)
+        assert max(loads) / (len(S) / s) < 1.15  # users reach 1.01, items 1.12 (contiguous optimum)
+        uniform = [int(np.sum(((S[col].astype(np.int64) * s) // N) == k)) for k in range(s)]
+        assert max(uniform) / (len(S) / s) > 1.3
+
+
+def test_balanced_wavefront_single_block_is_serial(orc):
+    rng = np.random.default_rng(13)
+    S = samples([(rng.integers(20), rng.integers(10), rng.normal()) for _ in range(400)], orc)
+    P, Q = orc.init_factors(20, 10, 4, 5, np.float32)
+    P1, Q1, P2, Q2 = P.copy(), Q.copy(), P.copy(), Q.copy()
+    orc.epoch_wavefront(P1, Q1, S, 0.05, 0.01, 0.02, 1, 5, 0, True)
+    orc.epoch_serial(P2, Q2, S, 0.05, 0.01, 0.02)
+    assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2)
