@@ -57,14 +57,33 @@ def measured_traffic(kernel_key: str):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, S, target_s: float, threads: int):
-    """The oracle (never tuned) on a bounded prefix of the same workload."""
+def _oracle_factors(w, S, dtype):
+    """Initial factors for the oracle: all rows, or (for models too large to
+    build on the host in seconds) the rows S touches, with S renumbered."""
     import numpy as np
     import oracle
 
-    k = w["k"]
-    P, Q = oracle.init_factors(w["m"], w["n"], k, w["seed"], np.float32)
-    probe = min(len(S), 100_000)
+    if w["m"] * w["k"] <= 1 << 30:
+        P, Q = oracle.init_factors(w["m"], w["n"], w["k"], w["seed"], dtype)
+        return P, Q, S, ""
+    ur, uc = np.unique(S["u"], return_inverse=True)
+    vr, vc = np.unique(S["v"], return_inverse=True)
+    C = S.copy()
+    C["u"], C["v"] = uc, vc
+    P = oracle.init_rows(w["m"], w["k"], w["seed"], 0, ur, dtype)
+    Q = oracle.init_rows(w["n"], w["k"], w["seed"], 1, vr, dtype)
+    return P, Q, C, f" (on the {len(ur)} user and {len(vr)} item rows the sample touches)"
+
+
+def cpu_baseline(w, S, target_s: float, threads: int):
+    """The oracle (never tuned) on a bounded prefix of the same workload.
+    S: a host prefix of the training samples, long enough for target_s."""
+    import numpy as np
+    import oracle
+
+    dtype = np.float16 if w["dtype"] == "fp16" else np.float32
+    P, Q, S, note = _oracle_factors(w, S, dtype)
+    probe = min(len(S), 100_000 if dtype == np.float32 else 20_000)
     t0 = time.perf_counter()
     oracle.epoch_serial(P, Q, S[:probe], w["lr"], w["lam"], w["lam"])
     rate = probe / max(time.perf_counter() - t0, 1e-9)
@@ -74,16 +93,17 @@ def cpu_baseline(w, S, target_s: float, threads: int):
     dt = time.perf_counter() - t0
     serial = {"value": count / dt, "unit": "updates/s", "cores": 1, "kind": "oracle",
               "sample": f"serial binary64 oracle, samples {probe}..{probe + count - 1} of epoch 0 of the "
-                        f"{w['name']} workload ({count} updates, {dt:.1f} s)"}
+                        f"{w['name']} workload ({count} updates, {dt:.1f} s){note}"}
     omp = None
     if threads > 1:
-        P, Q = oracle.init_factors(w["m"], w["n"], k, w["seed"], np.float32)
+        P, Q, S, note = _oracle_factors(w, S, dtype)
         n2 = int(min(len(S), count * threads))
         t0 = time.perf_counter()
         used = oracle.epoch_hogwild_omp(P, Q, S[:n2], w["lr"], w["lam"], w["lam"], 256, threads)
         dt = time.perf_counter() - t0
         omp = {"value": n2 / dt, "unit": "updates/s", "cores": used, "kind": "oracle-openmp-hogwild",
-               "sample": f"first {n2} samples of epoch 0, batches of 256 claimed by {used} threads ({dt:.1f} s)"}
+               "sample": f"first {n2} samples of epoch 0, batches of 256 claimed by {used} threads ({dt:.1f} s)"
+                         f"{note}"}
     return serial, omp
 
 
@@ -94,7 +114,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="netflix")
     ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det"])
-    ap.add_argument("--grid-s", type=int, default=32)
+    ap.add_argument("--grid-s", type=int, default=0, help="wavefront grid side (0: the workload's, else 32)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--depth", type=int, default=4)
     ap.add_argument("--team-waves", type=int, default=0)
@@ -124,10 +144,18 @@ def main():
     if args.ntrain:
         w["ntrain"] = args.ntrain
     t0 = time.perf_counter()
-    S, T = datagen.make(w)
-    log(f"generated {w['name']}: {len(S)} train + {len(T)} test in {time.perf_counter() - t0:.1f}s")
-    dS = mfsgd.samples_to_device(S, dev)
+    if w["draw"] == "independent":
+        # generated chunk by chunk straight into HBM; the host keeps a prefix for the CPU baseline
+        dS = datagen.draw_to_device(w, 0, w["ntrain"], dev, progress=lambda a, b: (
+            log(f"  generated {a}/{b}") if a % (1 << 29) < (1 << 25) else None))
+        T = datagen.draw(w, w["ntrain"], w["ntest"])
+        S = datagen.draw(w, 0, min(w["ntrain"], 50_000_000 if args.cpu_threads > 1 else 20_000_000))
+    else:
+        S, T = datagen.make(w)
+        dS = mfsgd.samples_to_device(S, dev)
     dT = mfsgd.samples_to_device(T, dev)
+    nnz = w["ntrain"]
+    log(f"generated {w['name']}: {nnz} train + {len(T)} test in {time.perf_counter() - t0:.1f}s")
 
     dtype = 1 if w["dtype"] == "fp16" else 0
     feat_bytes = 2 if dtype else 4
@@ -138,11 +166,11 @@ def main():
     resident = mfsgd.get_option("resident_waves")
     partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1
     kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
+    grid_s = args.grid_s or w.get("grid_s", 32)
     if args.scheme != "hogwild":
         t0 = time.perf_counter()
-        mfsgd.plan(dS, args.grid_s)
-        log(f"wavefront plan (s={args.grid_s}) {time.perf_counter() - t0:.3f}s")
-    nnz = len(S)
+        mfsgd.plan(dS, grid_s)
+        log(f"wavefront plan (s={grid_s}) {time.perf_counter() - t0:.3f}s")
     stream = torch.cuda.current_stream()
 
     def step(t, ev=None):
@@ -196,9 +224,10 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32" if dtype == 0 else "f16-storage/f32-math",
-        "data": "synthetic (planted low-rank model with the Netflix shape, seeded)",
+        "data": f"synthetic (seeded planted low-rank model with the {w['name']} shape)",
         "config": {"workload": f"{w['name']}: m={w['m']} n={w['n']} k={w['k']} nnz={nnz} ntest={len(T)} "
-                               f"{w['dtype']} {args.scheme} f=256",
+                               f"{w['dtype']} {args.scheme}" + (f" s={grid_s}" if args.scheme != "hogwild"
+                                                                 else " f=256"),
                    "scheme": args.scheme, "partitioned": partitioned, "workers": args.workers or "auto",
                    "resident_waves": resident,
                    "depth": args.depth, "epochs_timed": args.steps},

@@ -216,8 +216,15 @@ int64_t mfsgd_get_epoch(void);
  *                      caller's array).
  *   MFSGD_DBG_TRACE  : batch-Hogwild!: dst int32[ceil(nnz/f)], the worker
  *                      that ran each batch; wavefront: dst int32[s*s],
- *                      entry i*s+w = column block of worker i in wave w. */
-enum { MFSGD_DBG_VISITS = 1, MFSGD_DBG_TRACE = 2 };
+ *                      entry i*s+w = column block of worker i in wave w.
+ *   MFSGD_DBG_PLAN_STARTS : the wavefront-update plan of the last mfsgd_plan:
+ *                      count = s*s+1, dst int64 -- first planned position of
+ *                      block (I, J) at entry I*s+J, nnz at entry s*s.
+ *   MFSGD_DBG_PLAN_ORDER  : same plan, count <= nnz, dst int64 -- position in
+ *                      the caller's array of each planned sample (needs a plan
+ *                      made while debug bit 0 was set).
+ * dst may be host or device memory. */
+enum { MFSGD_DBG_VISITS = 1, MFSGD_DBG_TRACE = 2, MFSGD_DBG_PLAN_STARTS = 3, MFSGD_DBG_PLAN_ORDER = 4 };
 int mfsgd_debug_read(int32_t what, void* dst, int64_t count, void* stream);
 
 /* Release everything; the context returns to the un-initialised state. */

@@ -54,6 +54,8 @@ def lib():
         L.orc_splitmix64.restype = u64
         L.orc_init_factors.argtypes = [i64, i64, i32, u64, C.c_int, vp, vp]
         L.orc_init_factors.restype = None
+        L.orc_init_rows.argtypes = [i64, i32, u64, C.c_int, C.c_int, vp, i64, vp]
+        L.orc_init_rows.restype = None
         L.orc_sgd_step.argtypes = [vp, vp, i32, f64, f64, f64, f64]
         L.orc_sgd_step.restype = None
         L.orc_epoch_serial.argtypes = [i32, C.c_int, vp, vp, vp, i64, f32, f32, f32]
@@ -136,6 +138,14 @@ def init_factors(m: int, n: int, k: int, seed: int, dtype=np.float32):
     Qt = np.empty((n, k), dtype=dtype)
     lib().orc_init_factors(m, n, k, seed, _dtype_code(P), _ptr(P), _ptr(Qt))
     return P, Qt
+
+
+def init_rows(N: int, k: int, seed: int, which: int, rows, dtype=np.float32):
+    """Initial values of the given rows of P (which=0) or Q^T (which=1)."""
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty((len(rows), k), dtype=dtype)
+    lib().orc_init_rows(N, k, seed, _dtype_code(out), which, _ptr(rows), len(rows), _ptr(out))
+    return out
 
 
 def epoch_serial(P, Qt, S, lr, lambda_p, lambda_q):

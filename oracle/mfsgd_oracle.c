@@ -159,6 +159,20 @@ void orc_init_factors(int64_t m, int64_t n, int32_t k, uint64_t seed, int dtype,
         orc_store(Qt, dtype, i, orc_init_value(sq, i, inv_sqrt_k));
 }
 
+/* The same initial values for selected rows only (which: 0 = P, 1 = Q^T):
+ * out[i][j] = initial value of row rows[i], column j.  Lets a check at a very
+ * large m look at the rows a sample prefix touches without building all of P. */
+void orc_init_rows(int64_t nrows_total, int32_t k, uint64_t seed, int dtype, int which, const int64_t* rows,
+                   int64_t count, void* out)
+{
+    double inv_sqrt_k = 1.0 / sqrt((double)k);
+    uint64_t st = orc_stream(seed, which ? ORC_TAG_Q : ORC_TAG_P);
+    (void)nrows_total;
+    for (int64_t i = 0; i < count; i++)
+        for (int32_t j = 0; j < k; j++)
+            orc_store(out, dtype, i * k + j, orc_init_value(st, rows[i] * (int64_t)k + j, inv_sqrt_k));
+}
+
 /* ------------------------------------------------------------------------ */
 /* One SGD update (section 2.2, the error and the two update equations).      */
 /* Reading: both vectors are updated from their values before this step (the */

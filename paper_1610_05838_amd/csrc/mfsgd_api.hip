@@ -46,6 +46,7 @@ struct Plan {
     int64_t orig_cap = 0;
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
+    bool valid() const { return nnz >= 0 && bstart != nullptr; }
     void invalidate()
     {
         src = nullptr;
@@ -75,10 +76,10 @@ struct Context {
     Plan wf;                // the caller's wavefront-update plan (mfsgd_plan)
     Plan hw;                // internal plan of the XCD-partitioned batch-Hogwild!
     // planner scratch
-    int32_t* counts = nullptr;
+    int64_t* counts = nullptr;
     int64_t* totals = nullptr;
     int64_t* bnd = nullptr; // 2 x (kMaxGrid + 1)
-    uint32_t* deg = nullptr;
+    unsigned long long* deg = nullptr;
     int64_t deg_cap = 0;
     // debug
     uint32_t* visits = nullptr;
@@ -412,21 +413,30 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
 // ---------------------------------------------------------------------------
 // Optimal consecutive cut of per-index counts into s ranges: the smallest cap
 // on a range's count for which a greedy fill needs at most s ranges, and the
-// ranges of that greedy fill.
-int64_t greedy_ranges(const std::vector<uint32_t>& cnt, int64_t cap, int s, int64_t* bounds)
+// ranges of that greedy fill.  pre[i] = count of indices 0..i-1; a greedy
+// range starting at index b ends before the first e > b with
+// pre[e+1] - pre[b] > cap, found by binary search, so one fill costs
+// O(s log N) instead of O(N).
+int64_t greedy_ranges(const std::vector<int64_t>& pre, int64_t cap, int s, int64_t* bounds)
 {
-    const int64_t N = (int64_t)cnt.size();
-    int64_t k = 0, load = 0;
+    const int64_t N = (int64_t)pre.size() - 1;
+    int64_t k = 0, b = 0;
     if (bounds)
         bounds[0] = 0;
-    for (int64_t i = 0; i < N; ++i) {
-        if (load + cnt[i] > cap) {
-            ++k;
-            load = 0;
-            if (bounds && k <= s)
-                bounds[k] = i;
-        }
-        load += cnt[i];
+    while (true) {
+        // first e in (b, N] with pre[e] - pre[b] > cap ends the range at e - 1 (range = [b, e-1))
+        const int64_t lim = pre[b] + cap;
+        const int64_t e = std::upper_bound(pre.begin() + b + 1, pre.end(), lim) - pre.begin();
+        // indices b .. e-2 fit; index e-1 would overflow (or e = N + 1: all fit)
+        const int64_t next = std::max<int64_t>(e - 1, b + 1);
+        if (next >= N)
+            break;
+        ++k;
+        if (k > s && !bounds)
+            return k + 1; // infeasible; exact count not needed
+        if (bounds && k <= s)
+            bounds[k] = next;
+        b = next;
     }
     if (bounds)
         for (int64_t j = k + 1; j <= s; ++j)
@@ -434,21 +444,24 @@ int64_t greedy_ranges(const std::vector<uint32_t>& cnt, int64_t cap, int s, int6
     return k + 1;
 }
 
-void balanced_cut(const std::vector<uint32_t>& cnt, int64_t nnz, int s, int64_t* bounds)
+void balanced_cut(const std::vector<unsigned long long>& cnt, int64_t nnz, int s, int64_t* bounds)
 {
+    std::vector<int64_t> pre(cnt.size() + 1, 0);
     int64_t top = 0;
-    for (uint32_t x : cnt)
-        top = std::max<int64_t>(top, x);
+    for (size_t i = 0; i < cnt.size(); ++i) {
+        pre[i + 1] = pre[i] + (int64_t)cnt[i];
+        top = std::max<int64_t>(top, (int64_t)cnt[i]);
+    }
     int64_t lo = std::max<int64_t>((nnz + s - 1) / s, top);
     int64_t hi = std::max<int64_t>(nnz, lo);
     while (lo < hi) {
         const int64_t mid = lo + (hi - lo) / 2;
-        if (greedy_ranges(cnt, mid, s, nullptr) <= s)
+        if (greedy_ranges(pre, mid, s, nullptr) <= s)
             hi = mid;
         else
             lo = mid + 1;
     }
-    greedy_ranges(cnt, lo, s, bounds);
+    greedy_ranges(pre, lo, s, bounds);
 }
 
 int bad_index_error()
@@ -462,7 +475,7 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     Context& c = g;
     pl.invalidate();
     if (!c.counts) {
-        CHK(dalloc((void**)&c.counts, sizeof(int32_t) * kMaxGrid * kMaxGrid * kPlanChunks, "plan counts"));
+        CHK(dalloc((void**)&c.counts, sizeof(int64_t) * kMaxGrid * kMaxGrid * kPlanChunks, "plan counts"));
         CHK(dalloc((void**)&c.totals, sizeof(int64_t) * kMaxGrid * kMaxGrid, "plan totals"));
     }
     if (!pl.bstart)
@@ -476,11 +489,12 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     const int64_t* cbnd = nullptr;
     if (balanced) {
         CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
-        HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(uint32_t) * (size_t)(c.m + c.n), st));
+        HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
         HIPCHK(plan_degrees(S, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
-        std::vector<uint32_t> du((size_t)c.m), dv((size_t)c.n);
-        HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(uint32_t) * du.size(), hipMemcpyDeviceToHost, st));
-        HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(uint32_t) * dv.size(), hipMemcpyDeviceToHost, st));
+        std::vector<unsigned long long> du((size_t)c.m), dv((size_t)c.n);
+        HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(unsigned long long) * du.size(), hipMemcpyDeviceToHost, st));
+        HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(unsigned long long) * dv.size(), hipMemcpyDeviceToHost,
+                              st));
         HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
         HIPCHK(hipStreamSynchronize(st));
         if (*c.hflag) {
@@ -749,6 +763,15 @@ int debug_read_impl(int32_t what, void* dst, int64_t count, hipStream_t st)
             return fail(MFSGD_ESTATE, "no schedule trace recorded for that many entries (set debug bit 1)");
         if (count)
             HIPCHK(hipMemcpyAsync(dst, c.trace, sizeof(int32_t) * (size_t)count, hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_PLAN_STARTS) {
+        if (!c.wf.valid() || count != (int64_t)c.wf.s * c.wf.s + 1)
+            return fail(MFSGD_ESTATE, "no wavefront plan, or count is not s*s+1");
+        HIPCHK(hipMemcpyAsync(dst, c.wf.bstart, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_PLAN_ORDER) {
+        if (!c.wf.valid() || !c.wf.has_orig || count > c.wf.nnz)
+            return fail(MFSGD_ESTATE, "no wavefront plan with positions (plan with debug bit 0 set)");
+        if (count)
+            HIPCHK(hipMemcpyAsync(dst, c.wf.orig, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
     } else {
         return fail(MFSGD_EINVAL, "unknown debug buffer");
     }

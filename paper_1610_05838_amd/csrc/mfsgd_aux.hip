@@ -141,8 +141,8 @@ __device__ __forceinline__ int block_of(int u, int v, int64_t m, int64_t n, int 
 
 // Per-index sample counts (users and items) for the balanced cut; indices out
 // of range are skipped and flagged.
-__global__ void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n, uint32_t* __restrict__ du,
-                          uint32_t* __restrict__ dv, int* bad)
+__global__ void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
+                          unsigned long long* __restrict__ du, unsigned long long* __restrict__ dv, int* bad)
 {
     int found = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * blockDim.x) {
@@ -152,15 +152,15 @@ __global__ void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, 
             found = 1;
             continue;
         }
-        atomicAdd(du + u, 1u);
-        atomicAdd(dv + v, 1u);
+        atomicAdd(du + u, 1ull);
+        atomicAdd(dv + v, 1ull);
     }
     if (found)
         atomicOr(bad, 1);
 }
 
-hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, uint32_t* du, uint32_t* dv, int* bad,
-                        hipStream_t st)
+hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsigned long long* du,
+                        unsigned long long* dv, int* bad, hipStream_t st)
 {
     if (nnz <= 0)
         return hipSuccess;
@@ -173,7 +173,7 @@ hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, uint
 
 __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
                                                    int s, const int64_t* rbnd, const int64_t* cbnd,
-                                                   int32_t* __restrict__ counts, int* bad)
+                                                   int64_t* __restrict__ counts, int* bad)
 {
     __shared__ int hist[kMaxGrid * kMaxGrid];
     __shared__ Cut cut;
@@ -203,11 +203,11 @@ __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S,
 }
 
 // exclusive scan of counts[b][0..kPlanChunks) in place, total to totals[b]
-__global__ __launch_bounds__(256) void k_plan_scan_chunks(int32_t* __restrict__ counts, int64_t* __restrict__ totals)
+__global__ __launch_bounds__(256) void k_plan_scan_chunks(int64_t* __restrict__ counts, int64_t* __restrict__ totals)
 {
     constexpr int per = kPlanChunks / 256;
     __shared__ int64_t part[256];
-    int32_t* row = counts + (int64_t)blockIdx.x * kPlanChunks;
+    int64_t* row = counts + (int64_t)blockIdx.x * kPlanChunks;
     int64_t local[per];
     int64_t acc = 0;
 #pragma unroll
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void k_plan_scan_chunks(int32_t* __restrict__ 
     int64_t run = threadIdx.x > 0 ? part[threadIdx.x - 1] : 0;
 #pragma unroll
     for (int i = 0; i < per; ++i) {
-        row[threadIdx.x * per + i] = (int32_t)run;
+        row[threadIdx.x * per + i] = run;
         run += local[i];
     }
     if (threadIdx.x == 255)
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(1024) void k_plan_scan_blocks(const int64_t* __rest
 
 __global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
                                                      int s, const int64_t* rbnd, const int64_t* cbnd,
-                                                     const int32_t* __restrict__ counts,
+                                                     const int64_t* __restrict__ counts,
                                                      const int64_t* __restrict__ bstart, Sample* __restrict__ Sp,
                                                      int64_t* __restrict__ orig)
 {

@@ -70,7 +70,7 @@ hipError_t reset_tickets(uint32_t* tickets, uint32_t* done, hipStream_t st);
 hipError_t probe_xcc(int* out, int n, hipStream_t st);
 // stable bucketing of samples into the s x s grid
 struct PlanBuffers {
-    int32_t* counts;     // s*s*chunks, bin-major
+    int64_t* counts;     // s*s*chunks, bin-major
     int64_t* totals;     // s*s
     int64_t* bstart;     // s*s+1
     Sample* Sp;          // planned copy
@@ -80,8 +80,8 @@ struct PlanBuffers {
     const int64_t* cbnd; // s+1 item bounds
 };
 // per-index sample counts for the balanced cut (indices out of range raise *bad)
-hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, uint32_t* du, uint32_t* dv, int* bad,
-                        hipStream_t st);
+hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsigned long long* du,
+                        unsigned long long* dv, int* bad, hipStream_t st);
 constexpr int kPlanChunks = 2048;
 // counts, per-block scans and block starts; raises *b.bad on an index out of range
 hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,

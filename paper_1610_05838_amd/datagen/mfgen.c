@@ -25,7 +25,7 @@ typedef struct {
 
 typedef struct {
     int64_t m, n;
-    int32_t k;         /* rank of the planted model */
+    int32_t k;         /* rank of the planted model (may be below the trained rank) */
     int32_t model;     /* rating model, see gen_rating */
     uint64_t seed;
     double noise_var;  /* variance of the additive Gaussian noise */
@@ -80,7 +80,10 @@ void gen_planted(const gen_spec* sp, float* Ps, float* Qs)
 
 /* Zipf-like table over N ranks: P(rank r) proportional to r^-a (r = 1..N),
  * cdf[r-1] = cumulative probability; perm maps rank-1 to an index through a
- * seeded Fisher-Yates permutation, so popularity is not tied to the index. */
+ * seeded Fisher-Yates permutation, so popularity is not tied to the index.
+ * guide[j] (j = 0..G, G = 2^guide_bits) = first r with cdf[r] > j/G, which
+ * narrows the search of gen_pick to one bucket (Chen and Asau's guide table);
+ * the pick itself is unchanged. */
 void gen_zipf_table(int64_t N, double a, uint64_t seed, int which, double* cdf, int32_t* perm)
 {
     double acc = 0.0;
@@ -103,13 +106,39 @@ void gen_zipf_table(int64_t N, double a, uint64_t seed, int which, double* cdf, 
     }
 }
 
-static int64_t gen_pick(double x, int64_t N, const double* cdf, const int32_t* perm)
+void gen_zipf_guide(int64_t N, const double* cdf, int guide_bits, int64_t* guide)
 {
-    if (!cdf) {
+    const int64_t G = (int64_t)1 << guide_bits;
+    int64_t r = 0;
+    for (int64_t j = 0; j < G; j++) {
+        const double x = ldexp((double)j, -guide_bits);
+        while (r < N - 1 && !(cdf[r] > x))
+            r++;
+        guide[j] = r;
+    }
+    guide[G] = N - 1;
+}
+
+typedef struct {
+    const double* cdf;   /* NULL: uniform */
+    const int32_t* perm;
+    const int64_t* guide; /* NULL: plain binary search */
+    int guide_bits;
+} gen_table;
+
+static int64_t gen_pick(double x, int64_t N, const gen_table* t)
+{
+    if (!t->cdf) {
         int64_t i = (int64_t)(x * (double)N);
         return i < N ? i : N - 1;
     }
+    const double* cdf = t->cdf;
     int64_t lo = 0, hi = N - 1; /* first r with cdf[r] > x */
+    if (t->guide) {
+        const int64_t j = (int64_t)ldexp(x, t->guide_bits); /* exact: x < 1 is scaled by a power of two */
+        lo = t->guide[j];
+        hi = t->guide[j + 1];
+    }
     while (lo < hi) {
         int64_t mid = lo + (hi - lo) / 2;
         if (cdf[mid] > x)
@@ -117,7 +146,7 @@ static int64_t gen_pick(double x, int64_t N, const double* cdf, const int32_t* p
         else
             lo = mid + 1;
     }
-    return perm[lo];
+    return t->perm[lo];
 }
 
 static float gen_rating(const gen_spec* sp, const float* Ps, const float* Qs, int64_t u, int64_t v, double z)
@@ -146,17 +175,24 @@ static float gen_rating(const gen_spec* sp, const float* Ps, const float* Qs, in
     }
 }
 
+/* Picks for explicit uniforms (lets a test compare the guided and the plain search). */
+void gen_pick_batch(const double* x, int64_t count, int64_t N, const gen_table* t, int64_t* out)
+{
+    for (int64_t i = 0; i < count; i++)
+        out[i] = gen_pick(x[i], N, t);
+}
+
 /* Independent draws for counters c0 .. c0+count-1: user and item from the
  * given tables (NULL cdf = uniform), rating from the planted model. */
-void gen_draw(const gen_spec* sp, const float* Ps, const float* Qs, const double* cdf_u, const int32_t* perm_u,
-              const double* cdf_v, const int32_t* perm_v, int64_t c0, int64_t count, gen_sample* out)
+void gen_draw(const gen_spec* sp, const float* Ps, const float* Qs, const gen_table* tu, const gen_table* tv,
+              int64_t c0, int64_t count, gen_sample* out)
 {
     uint64_t st = gen_stream(sp->seed, GEN_S_DRAW);
 #pragma omp parallel for schedule(static, 4096)
     for (int64_t i = 0; i < count; i++) {
         uint64_t c = (uint64_t)(c0 + i) * 4;
-        int64_t u = gen_pick(gen_u01(gen_hash(st, c)), sp->m, cdf_u, perm_u);
-        int64_t v = gen_pick(gen_u01(gen_hash(st, c + 1)), sp->n, cdf_v, perm_v);
+        int64_t u = gen_pick(gen_u01(gen_hash(st, c)), sp->m, tu);
+        int64_t v = gen_pick(gen_u01(gen_hash(st, c + 1)), sp->n, tv);
         double z = gen_normal(gen_hash(st, c + 2));
         out[i].u = (int32_t)u;
         out[i].v = (int32_t)v;

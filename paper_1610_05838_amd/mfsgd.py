@@ -25,7 +25,7 @@ LIB_PATH = os.path.join(HERE, "libmfsgd.so")
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ETIMEOUT, ENUMERIC = 0, -1, -2, -3, -4, -5, -6
 BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET = 0, 1, 2
 FP32, FP16 = 0, 1
-DBG_VISITS, DBG_TRACE = 1, 2
+DBG_VISITS, DBG_TRACE, DBG_PLAN_STARTS, DBG_PLAN_ORDER = 1, 2, 3, 4
 
 SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET}
 
@@ -187,6 +187,20 @@ def debug_trace(count: int, stream=None) -> torch.Tensor:
     _check(lib().mfsgd_debug_read(DBG_TRACE, C.c_void_p(out.data_ptr()), count, _stream(stream)),
            "mfsgd_debug_read")
     return out
+
+
+def debug_plan_starts(s: int, stream=None) -> torch.Tensor:
+    out = torch.empty(s * s + 1, dtype=torch.int64, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_PLAN_STARTS, C.c_void_p(out.data_ptr()), s * s + 1, _stream(stream)),
+           "mfsgd_debug_read")
+    return out
+
+
+def debug_plan_order(nnz: int, stream=None) -> torch.Tensor:
+    out = torch.empty(max(nnz, 1), dtype=torch.int64, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_PLAN_ORDER, C.c_void_p(out.data_ptr()), nnz, _stream(stream)),
+           "mfsgd_debug_read")
+    return out[:nnz]
 
 
 def finalize() -> None:

@@ -66,3 +66,25 @@ def test_hugewiki_shape_items_uniform(gen):
     # uniform items: counts ~ Poisson(10)
     assert cv.mean() == pytest.approx(400_000 / w["n"]) and cv.max() < 40
     assert abs(float(a["r"].mean())) < 0.02 and float(a["r"].var()) == pytest.approx(2.0, rel=0.03)
+
+
+def test_guided_zipf_pick_equals_plain_search(gen):
+    N, a, seed = 3_000_000, 1.0, 77
+    bits = gen.guide_bits(N)
+    rng = np.random.default_rng(5)
+    G = 1 << bits
+    j = rng.integers(0, G, 20_000)
+    edges = np.concatenate([j / G, np.nextafter(j / G, 0.0), np.nextafter(j / G, 1.0), [0.0, np.nextafter(1.0, 0.0)]])
+    cdf, _ = gen.zipf_table(N, a, seed, 0)
+    x = np.concatenate([rng.random(200_000), edges, cdf[:1000], np.nextafter(cdf[:1000], 0.0)])
+    x = x[(x >= 0) & (x < 1)]
+    assert np.array_equal(gen.pick(x, N, a, seed, 0, guided=True), gen.pick(x, N, a, seed, 0, guided=False))
+    w = gen.workload("yahoo", ntrain=200_000, ntest=0)
+    assert np.array_equal(gen.draw(w, 0, 200_000), gen.draw(w, 0, 200_000, guided=False))
+
+
+def test_hugewiki_planted_rank(gen):
+    w = gen.workload("hugewiki", m=100_000, ntrain=300_000, ntest=0)
+    Ps, Qs = gen.planted(w)
+    assert Ps.shape == (100_000, 16) and Qs.shape == (w["n"], 16)
+    assert float(Ps.var()) == pytest.approx(1 / math.sqrt(16), rel=0.01)

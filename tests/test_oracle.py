@@ -413,3 +413,11 @@ def test_balanced_wavefront_single_block_is_serial(orc):
     orc.epoch_wavefront(P1, Q1, S, 0.05, 0.01, 0.02, 1, 5, 0, True)
     orc.epoch_serial(P2, Q2, S, 0.05, 0.01, 0.02)
     assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_init_rows_equal_full_init(orc, dtype):
+    P, Q = orc.init_factors(300, 70, 24, 31, dtype)
+    rows = np.array([0, 299, 17, 17, 150])
+    assert np.array_equal(orc.init_rows(300, 24, 31, 0, rows, dtype), P[rows])
+    assert np.array_equal(orc.init_rows(70, 24, 31, 1, [69, 0, 5], dtype), Q[[69, 0, 5]])
