@@ -111,7 +111,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  updates, so depth never changes the serial semantics of
  *                  one worker.
  *   "team_waves"   wavefronts per wavefront-update worker; 0 (default) = as
- *                  many as stay resident, divided over the s workers.
+ *                  many as stay resident, shared among the s workers in
+ *                  proportion to the samples of their row blocks (each
+ *                  worker on one XCD, the XCDs loaded as evenly as the row
+ *                  blocks allow).
  *   "partition"    batch-Hogwild!: 0 one address space, 1 partitioned over
  *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
  *                  partitioned when P and Q together take at most 64 MiB
@@ -142,7 +145,8 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
  * "partitioned" (whether batch-Hogwild! runs partitioned for this model),
  * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
- * block-scheduled kernel).
+ * block-scheduled kernel), "teams_grid" (workgroups of the last
+ * block-scheduled epoch, 0 before one).
  * Returns MFSGD_EINVAL for an unknown key or an out-of-range value. */
 int mfsgd_set_option(const char* key, int64_t value);
 int mfsgd_get_option(const char* key, int64_t* value);
@@ -223,8 +227,21 @@ int64_t mfsgd_get_epoch(void);
  *   MFSGD_DBG_PLAN_ORDER  : same plan, count <= nnz, dst int64 -- position in
  *                      the caller's array of each planned sample (needs a plan
  *                      made while debug bit 0 was set).
+ *   MFSGD_DBG_TEAM_MAP : the team layout of the last block-scheduled epoch:
+ *                      count = its workgroup count (read-only option
+ *                      "teams_grid"), dst int32 -- team << 16 | member of
+ *                      each workgroup, -1 for an idle one.
+ *   MFSGD_DBG_TEAM_SIZES : same layout, count = s, dst int32 -- workgroups
+ *                      of each team.
  * dst may be host or device memory. */
-enum { MFSGD_DBG_VISITS = 1, MFSGD_DBG_TRACE = 2, MFSGD_DBG_PLAN_STARTS = 3, MFSGD_DBG_PLAN_ORDER = 4 };
+enum {
+    MFSGD_DBG_VISITS = 1,
+    MFSGD_DBG_TRACE = 2,
+    MFSGD_DBG_PLAN_STARTS = 3,
+    MFSGD_DBG_PLAN_ORDER = 4,
+    MFSGD_DBG_TEAM_MAP = 5,
+    MFSGD_DBG_TEAM_SIZES = 6
+};
 int mfsgd_debug_read(int32_t what, void* dst, int64_t count, void* stream);
 
 /* Release everything; the context returns to the un-initialised state. */

@@ -45,6 +45,8 @@ struct Plan {
     int64_t* orig = nullptr;
     int64_t orig_cap = 0;
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
+    std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
+    uint64_t version = 0;        // bumped by every build
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
     bool valid() const { return nnz >= 0 && bstart != nullptr; }
     void invalidate()
@@ -86,6 +88,14 @@ struct Context {
     int64_t visits_cap = 0, visits_n = 0;
     int32_t* trace = nullptr;
     int64_t trace_cap = 0, trace_n = 0;
+    // team layout of the last block-scheduled launch (device copy in tmap/tsize)
+    int32_t* tmap = nullptr;
+    int64_t tmap_cap = 0;
+    int32_t* tsize = nullptr;
+    const Plan* lay_plan = nullptr;
+    uint64_t lay_version = 0;
+    int64_t lay_want = -1;
+    int lay_grid = 0, lay_waves = 0, lay_depth = 0;
 };
 
 Options g_opt;
@@ -190,6 +200,8 @@ void release_all()
     dfree(c.deg);
     dfree(c.visits);
     dfree(c.trace);
+    dfree(c.tmap);
+    dfree(c.tsize);
     c = Context();
 }
 
@@ -311,7 +323,8 @@ int get_option_impl(const char* key, int64_t* value)
             return MFSGD_OK;
         }
     const bool ro = !std::strcmp(key, "resident_waves") || !std::strcmp(key, "xcds") || !std::strcmp(key, "cus") ||
-                    !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned");
+                    !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
+                    !std::strcmp(key, "teams_grid");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
@@ -324,6 +337,8 @@ int get_option_impl(const char* key, int64_t* value)
         *value = occupancy_blocked(g.KP, g.dtype, (int)g_opt.depth, 256);
     else if (!std::strcmp(key, "partitioned"))
         *value = partitioned_hogwild() ? 1 : 0;
+    else if (!std::strcmp(key, "teams_grid"))
+        *value = g.lay_plan ? g.lay_grid : 0;
     else
         *value = g.cus;
     return MFSGD_OK;
@@ -517,7 +532,11 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     if (bad)
         return bad_index_error();
     HIPCHK(plan_scatter(S, nnz, c.m, c.n, s, b, st));
+    pl.hstart.assign((size_t)s * s + 1, 0);
+    HIPCHK(hipMemcpyAsync(pl.hstart.data(), pl.bstart, sizeof(int64_t) * pl.hstart.size(), hipMemcpyDeviceToHost,
+                          st));
     HIPCHK(hipStreamSynchronize(st));
+    pl.version += 1;
     pl.src = samples;
     pl.nnz = nnz;
     pl.s = s;
@@ -557,36 +576,135 @@ int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
 // ---------------------------------------------------------------------------
 // epochs
 // ---------------------------------------------------------------------------
-// Team shape of a block-scheduled launch with grid side s and `want` waves per
-// team (0: as many as stay co-resident).  One-wavefront teams are single
-// workgroups placed anywhere; larger teams are workgroups of 4 wavefronts,
-// spread over the XCDs so that each team lives on one XCD.
-int team_layout(int s, int64_t want, EpochLaunch& a)
+// Team layout of a block-scheduled launch: which workgroup serves which
+// team.  Teams go to XCDs largest row block first, each onto the XCD with the
+// fewest samples so far; then each XCD's workgroup slots are shared among its
+// teams: one each, the rest in proportion to the samples of the team's row
+// block (largest remainders first), or `uniform` per team if uniform > 0.
+// Slot j of XCD x is workgroup j * nx + x (round-robin dispatch).
+struct TeamLayout {
+    std::vector<int32_t> tmap, tsize;
+    int64_t grid = 0;
+};
+
+int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, int64_t uniform, TeamLayout& L)
+{
+    const int s = (int)load.size();
+    std::vector<int> order(s), xcd(s);
+    for (int t = 0; t < s; ++t)
+        order[t] = t;
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return load[x] > load[y]; });
+    std::vector<int64_t> xl(nx, 0), xc(nx, 0);
+    for (int t : order) {
+        int best = 0;
+        for (int x = 1; x < nx; ++x)
+            if (xl[x] < xl[best] || (xl[x] == xl[best] && xc[x] < xc[best]))
+                best = x;
+        xcd[t] = best;
+        xl[best] += load[t];
+        xc[best] += 1;
+    }
+    for (int x = 0; x < nx; ++x)
+        if (xc[x] > slots)
+            return fail(MFSGD_EINVAL, "grid side exceeds the co-resident workgroup count");
+    L.tsize.assign(s, 1);
+    if (uniform > 0) {
+        int64_t G = uniform;
+        for (int x = 0; x < nx; ++x)
+            if (xc[x] > 0)
+                G = std::min<int64_t>(G, slots / xc[x]);
+        for (int t = 0; t < s; ++t)
+            L.tsize[t] = (int32_t)G;
+    } else {
+        for (int x = 0; x < nx; ++x) {
+            if (xc[x] == 0)
+                continue;
+            const int64_t spare = slots - xc[x];
+            std::vector<std::pair<double, int>> rem;
+            int64_t used = 0;
+            for (int t = 0; t < s; ++t) {
+                if (xcd[t] != x)
+                    continue;
+                const double share = xl[x] > 0 ? (double)spare * (double)load[t] / (double)xl[x]
+                                               : (double)spare / (double)xc[x];
+                const int64_t gi = std::min<int64_t>((int64_t)share, spare - used);
+                L.tsize[t] = (int32_t)(1 + gi);
+                used += gi;
+                rem.push_back({share - (double)gi, t});
+            }
+            std::stable_sort(rem.begin(), rem.end(),
+                             [](const std::pair<double, int>& p, const std::pair<double, int>& q) {
+                                 return p.first > q.first;
+                             });
+            for (size_t i = 0; used < spare && i < rem.size(); ++i, ++used)
+                L.tsize[rem[i].second] += 1;
+        }
+    }
+    std::vector<int64_t> fill(nx, 0);
+    for (int t = 0; t < s; ++t)
+        fill[xcd[t]] += L.tsize[t];
+    const int64_t rows = *std::max_element(fill.begin(), fill.end());
+    L.grid = rows * nx;
+    L.tmap.assign((size_t)L.grid, -1);
+    std::fill(fill.begin(), fill.end(), 0);
+    for (int t = 0; t < s; ++t)
+        for (int m = 0; m < L.tsize[t]; ++m) {
+            const int x = xcd[t];
+            L.tmap[(size_t)(fill[x] * nx + x)] = (t << 16) | m;
+            fill[x] += 1;
+        }
+    return MFSGD_OK;
+}
+
+// Team shape of a block-scheduled launch on plan pl with `want` wavefronts per
+// team (1: one-wavefront teams placed anywhere; 0: every co-resident slot,
+// shared in proportion to the row blocks' samples).
+int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
 {
     Context& c = g;
-    if (want == 1) {
-        a.nx = 1;
-        a.wg_waves = 1;
-        a.wg_per_team = 1;
-        return MFSGD_OK;
+    const int s = pl.s;
+    const int waves = want == 1 ? 1 : 4;
+    if (c.lay_plan != &pl || c.lay_version != pl.version || c.lay_want != want || c.lay_waves != waves ||
+        c.lay_depth != a.depth) {
+        TeamLayout L;
+        if (want == 1) {
+            L.grid = s;
+            L.tsize.assign(s, 1);
+            L.tmap.resize(s);
+            for (int t = 0; t < s; ++t)
+                L.tmap[t] = t << 16;
+        } else {
+            const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 64 * waves);
+            if (per_cu <= 0)
+                return fail(MFSGD_EHIP, "occupancy query failed for the block-scheduled kernel");
+            // Every workgroup of this persistent grid must be resident at once
+            // (teams wait on each other).  Measured on MI355X, fewer workgroups
+            // fit than the occupancy query reports (about 5.3 of 7 per CU), so
+            // only half of the reported count is used.  A grid that still did
+            // not fit would end in MFSGD_ETIMEOUT, not a hang.
+            const int64_t cap = (int64_t)std::max(1, per_cu / 2) * c.cus;
+            const int nx = std::max(1, c.nx);
+            std::vector<int64_t> load(s);
+            for (int t = 0; t < s; ++t)
+                load[t] = pl.hstart[(size_t)(t + 1) * s] - pl.hstart[(size_t)t * s];
+            CHK(build_team_layout(load, nx, cap / nx, want > 0 ? (want + 3) / 4 : 0, L));
+        }
+        CHK(grow(&c.tmap, &c.tmap_cap, L.grid, "team map"));
+        if (!c.tsize)
+            CHK(dalloc((void**)&c.tsize, sizeof(int32_t) * kMaxGrid, "team sizes"));
+        HIPCHK(hipMemcpy(c.tmap, L.tmap.data(), sizeof(int32_t) * L.tmap.size(), hipMemcpyHostToDevice));
+        HIPCHK(hipMemcpy(c.tsize, L.tsize.data(), sizeof(int32_t) * L.tsize.size(), hipMemcpyHostToDevice));
+        c.lay_plan = &pl;
+        c.lay_version = pl.version;
+        c.lay_want = want;
+        c.lay_waves = waves;
+        c.lay_depth = a.depth;
+        c.lay_grid = (int)L.grid;
     }
-    const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 256);
-    if (per_cu <= 0)
-        return fail(MFSGD_EHIP, "occupancy query failed for the block-scheduled kernel");
-    // Every workgroup of this persistent grid must be resident at once (teams
-    // wait on each other).  Measured on MI355X, fewer workgroups fit than the
-    // occupancy query reports (about 5.3 of 7 per CU), so only half of the
-    // reported count is used; 3-4K wavefronts already saturate the memory
-    // system.  A grid that still did not fit would end in MFSGD_ETIMEOUT,
-    // not a hang.
-    const int64_t cap = (int64_t)std::max(1, per_cu / 2) * c.cus; // co-resident workgroups
-    if (cap < s)
-        return fail(MFSGD_EINVAL, "grid side exceeds the co-resident workgroup count");
-    int64_t G = want > 0 ? (want + 3) / 4 : cap / s;
-    G = std::max<int64_t>(1, std::min<int64_t>(G, cap / s));
-    a.nx = (c.nx > 1 && s % c.nx == 0) ? c.nx : 1;
-    a.wg_waves = 4;
-    a.wg_per_team = (int)G;
+    a.grid = c.lay_grid;
+    a.tmap = c.tmap;
+    a.tsize = c.tsize;
+    a.wg_waves = waves;
     return MFSGD_OK;
 }
 
@@ -680,7 +798,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.S = pl->Sp;
         a.bstart = pl->bstart;
         a.s = s;
-        CHK(team_layout(s, want, a));
+        CHK(team_layout(*pl, want, a));
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;
@@ -772,6 +890,15 @@ int debug_read_impl(int32_t what, void* dst, int64_t count, hipStream_t st)
             return fail(MFSGD_ESTATE, "no wavefront plan with positions (plan with debug bit 0 set)");
         if (count)
             HIPCHK(hipMemcpyAsync(dst, c.wf.orig, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_TEAM_MAP || what == MFSGD_DBG_TEAM_SIZES) {
+        if (!c.lay_plan)
+            return fail(MFSGD_ESTATE, "no block-scheduled epoch has run");
+        const int64_t have = what == MFSGD_DBG_TEAM_MAP ? c.lay_grid : c.lay_plan->s;
+        if (count > have)
+            return fail(MFSGD_ESTATE, "count exceeds the team layout");
+        if (count)
+            HIPCHK(hipMemcpyAsync(dst, what == MFSGD_DBG_TEAM_MAP ? c.tmap : c.tsize, sizeof(int32_t) * (size_t)count,
+                                  hipMemcpyDefault, st));
     } else {
         return fail(MFSGD_EINVAL, "unknown debug buffer");
     }

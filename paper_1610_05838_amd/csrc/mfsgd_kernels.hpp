@@ -38,33 +38,37 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 // last member to finish releases it with w+1 (every column is used by exactly
 // one team per wave, so a ticket counts the waves completed on its column).
 //
-// A team is G workgroups; inside a block its G*blockDim/64 wavefronts run
+// A team is a set of workgroups; inside a block its wavefronts run
 // batch-Hogwild! (run_worker) over the block's samples.  Members do not wait
 // for each other between waves (they share the team's row block, which no
-// other team touches); the last one to finish a wave releases its column.  Team placement
-// follows the hardware: workgroup b runs on XCD b mod nx (round-robin
-// dispatch, checked at init), and every member of a team sits on one XCD, so
-// the team's unsynchronised updates meet in that XCD's shared L2.  Feature
-// rows move between teams only at block hand-over, through an agent-scope
-// release (L2 write-back) and acquire (L1/L2 invalidate), whichever XCDs the
-// two teams run on.  With nx = 1 the layout is placement-agnostic (used for
-// one-wavefront teams).
+// other team touches); the last one to finish a wave releases its column.
+// tmap[b] gives the team and member index of workgroup b (-1: idle), tsize[i]
+// the workgroup count of team i.  The host builds the map so that every
+// member of a team sits on one XCD (workgroup b runs on XCD b mod nx, checked
+// at init) and teams get workgroups in proportion to their row block's
+// samples; the team's unsynchronised updates then meet in that XCD's shared
+// L2.  Feature rows move between teams only at block hand-over, through an
+// agent-scope release (L2 write-back) and acquire (L1/L2 invalidate),
+// whichever XCDs the two teams run on.
 //
 // A ticket wait that exceeds spin_limit polls raises *err; every waiting
 // workgroup then leaves, so the grid always drains.
 template <int KP, typename T, int D, bool DBG>
 __global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
-                                                  int s, int nx, int tpx, int G, uint64_t sigma_c, uint64_t sigma_o,
+                                                  int s, const int32_t* __restrict__ tmap,
+                                                  const int32_t* __restrict__ tsize, uint64_t sigma_c, uint64_t sigma_o,
                                                   T* __restrict__ P, T* __restrict__ Q, float lr, float lp, float lq,
                                                   int f, uint32_t* tickets, uint32_t* done, uint32_t spin_limit,
                                                   int* err, DebugSink dbg, int32_t* trace)
 {
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
     __shared__ int abort_all;
-    const int xcc = (int)(blockIdx.x % (unsigned)nx);
-    const int idx = (int)(blockIdx.x / (unsigned)nx);
-    const int team = (idx % tpx) * nx + xcc;
-    const int member = idx / tpx;
+    const int tm = tmap[blockIdx.x];
+    if (tm < 0)
+        return;
+    const int team = tm >> 16;
+    const int member = tm & 0xffff;
+    const int G = tsize[team];
     const int waves = blockDim.x >> 6;
     const int wv = uniform(threadIdx.x >> 6);
     const int64_t W = (int64_t)G * waves;
@@ -225,9 +229,8 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
                            a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
-        const unsigned grid = (unsigned)(a.s * a.wg_per_team);
-        hipLaunchKernelGGL((k_blocked<KP, T, D, DBG>), dim3(grid), dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s,
-                           a.nx, a.s / a.nx, a.wg_per_team, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f,
+        hipLaunchKernelGGL((k_blocked<KP, T, D, DBG>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0, st, a.S,
+                           a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f,
                            a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave);
     }
     return hipGetLastError();

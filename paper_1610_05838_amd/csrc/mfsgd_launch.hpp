@@ -29,11 +29,13 @@ struct EpochLaunch {
     float lr, lp, lq;
     int sync_every;  // one-address-space batch-Hogwild!: batches between XCD cache flushes (0 = none)
     int sync_l1;     // ... and whether the other wavefronts drop their CU's L1 then
+    int nx;          // XCDs (one-address-space batch-Hogwild!: the first nx workgroups lead the flushes)
     // block-scheduled epochs
     const int64_t* bstart;
     int s;           // grid side
-    int nx;          // coherence domains (XCDs) the teams are spread over; s % nx == 0
-    int wg_per_team; // workgroups per team
+    int grid;        // workgroups launched
+    const int32_t* tmap;  // per workgroup: team << 16 | member, or -1 (idle)
+    const int32_t* tsize; // per team: its workgroup count
     int wg_waves;    // wavefronts per workgroup
     uint64_t sigma_c, sigma_o;
     uint32_t* tickets;

@@ -25,7 +25,7 @@ LIB_PATH = os.path.join(HERE, "libmfsgd.so")
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ETIMEOUT, ENUMERIC = 0, -1, -2, -3, -4, -5, -6
 BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET = 0, 1, 2
 FP32, FP16 = 0, 1
-DBG_VISITS, DBG_TRACE, DBG_PLAN_STARTS, DBG_PLAN_ORDER = 1, 2, 3, 4
+DBG_VISITS, DBG_TRACE, DBG_PLAN_STARTS, DBG_PLAN_ORDER, DBG_TEAM_MAP, DBG_TEAM_SIZES = 1, 2, 3, 4, 5, 6
 
 SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET}
 
@@ -201,6 +201,19 @@ def debug_plan_order(nnz: int, stream=None) -> torch.Tensor:
     _check(lib().mfsgd_debug_read(DBG_PLAN_ORDER, C.c_void_p(out.data_ptr()), nnz, _stream(stream)),
            "mfsgd_debug_read")
     return out[:nnz]
+
+
+def debug_team_layout(s: int, stream=None):
+    """(map, sizes) of the last block-scheduled epoch: per workgroup
+    team << 16 | member (-1 idle), per team its workgroup count."""
+    grid = get_option("teams_grid")
+    tmap = torch.empty(max(grid, 1), dtype=torch.int32, device="cuda")
+    sizes = torch.empty(s, dtype=torch.int32, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_TEAM_MAP, C.c_void_p(tmap.data_ptr()), grid, _stream(stream)),
+           "mfsgd_debug_read")
+    _check(lib().mfsgd_debug_read(DBG_TEAM_SIZES, C.c_void_p(sizes.data_ptr()), s, _stream(stream)),
+           "mfsgd_debug_read")
+    return tmap[:grid], sizes
 
 
 def finalize() -> None:

@@ -185,6 +185,40 @@ def test_xcd_layout_detected(M):
     assert x >= 1 and M.get_option("cus") % x == 0
 
 
+@pytest.mark.parametrize("s", [16, 5])
+def test_team_layout_follows_row_loads(M, s):
+    """Wavefront-update teams: each on one XCD, every member present once,
+    workgroups in proportion to the samples of the team's row block."""
+    rng = np.random.default_rng(3)
+    m, n = 64_000, 5_000
+    S = rand_samples(rng, m, n, 400_000)
+    S["u"][:300_000] = rng.integers(0, m // s, 300_000)  # row block 0 holds most samples
+    setup(M, m, n, 32, 5, balance=0)
+    d = M.samples_to_device(S)
+    M.plan(d, s)
+    M.epoch(d, 0.01, 0.05, 0.05, "wavefront")
+    tmap, sizes = (x.cpu().numpy() for x in M.debug_team_layout(s))
+    nx = M.get_option("xcds")
+    starts = M.debug_plan_starts(s).cpu().numpy()
+    load = starts[s::s] - starts[:-1:s]
+    xcd = {}
+    members = {t: [] for t in range(s)}
+    for b, e in enumerate(tmap):
+        if e < 0:
+            continue
+        t, mem = int(e) >> 16, int(e) & 0xFFFF
+        assert xcd.setdefault(t, b % nx) == b % nx
+        members[t].append(mem)
+    for t in range(s):
+        assert sorted(members[t]) == list(range(sizes[t])) and sizes[t] >= 1
+    assert int(np.argmax(load)) == 0 and sizes[0] == sizes.max()
+    # row block 0 holds more than an XCD's share of the samples: its team has an XCD to itself
+    assert [t for t in range(s) if xcd[t] == xcd[0]] == [0]
+    if s >= 2 * nx:
+        assert sizes[0] >= 2 * np.median(sizes)
+    assert len(set(xcd.values())) == min(s, nx)
+
+
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 def test_partitioned_hogwild_single_wave_teams_match_oracle(M, gen, dtype):
     """Partitioned batch-Hogwild! with one wavefront per team is the wavefront
