@@ -135,6 +135,13 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  L1 at those points (default 0).
  *   "spin_limit"   polls of a column ticket before the wait gives up with
  *                  MFSGD_ETIMEOUT (default 2^24, each poll sleeps briefly).
+ *   "skip_stores"  block-scheduled epochs: a wavefront that updates a row
+ *                  again within its in-flight window writes it back once per
+ *                  run (the final values are the same).  0 never, 1 always,
+ *                  2 (default) when one item holds more than half of the
+ *                  samples of its column block (every worker passes through
+ *                  that column each epoch).  Epochs with debug output never
+ *                  skip.
  *   "debug"        bit 0: count visits of every sample (read with
  *                  mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
  *                  schedule (MFSGD_DBG_TRACE).  Costs one extra atomic per

@@ -30,6 +30,7 @@ struct Options {
     int64_t sync_every = 0;
     int64_t sync_l1 = 0;
     int64_t spin_limit = int64_t(1) << 24;
+    int64_t skip_stores = 2;
     int64_t debug = 0;
 };
 
@@ -46,6 +47,7 @@ struct Plan {
     int64_t orig_cap = 0;
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
+    double hot_col = 0.0;        // largest share of a column block's samples held by one item
     uint64_t version = 0;        // bumped by every build
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
     bool valid() const { return nnz >= 0 && bstart != nullptr; }
@@ -92,6 +94,8 @@ struct Context {
     int32_t* tmap = nullptr;
     int64_t tmap_cap = 0;
     int32_t* tsize = nullptr;
+    unsigned char* sink = nullptr; // rows for skipped stores, 2 per wavefront of the grid
+    int64_t sink_cap = 0;
     const Plan* lay_plan = nullptr;
     uint64_t lay_version = 0;
     int64_t lay_want = -1;
@@ -202,6 +206,7 @@ void release_all()
     dfree(c.trace);
     dfree(c.tmap);
     dfree(c.tsize);
+    dfree(c.sink);
     c = Context();
 }
 
@@ -290,6 +295,7 @@ const OptSpec kOpts[] = {
     {"sync_every", &Options::sync_every, 0, int64_t(1) << 30, "sync_every must be in [0, 2^30]"},
     {"sync_l1", &Options::sync_l1, 0, 1, "sync_l1 must be 0 or 1"},
     {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
+    {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
 };
 
@@ -502,26 +508,45 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
     const int64_t* rbnd = nullptr;
     const int64_t* cbnd = nullptr;
+    // per-index sample counts: the balanced cut needs both, the hot-column
+    // measure below the items'
+    CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
+    HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
+    HIPCHK(plan_degrees(S, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
+    std::vector<unsigned long long> du, dv((size_t)c.n);
     if (balanced) {
-        CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
-        HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
-        HIPCHK(plan_degrees(S, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
-        std::vector<unsigned long long> du((size_t)c.m), dv((size_t)c.n);
+        du.resize((size_t)c.m);
         HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(unsigned long long) * du.size(), hipMemcpyDeviceToHost, st));
-        HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(unsigned long long) * dv.size(), hipMemcpyDeviceToHost,
-                              st));
-        HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
-        HIPCHK(hipStreamSynchronize(st));
-        if (*c.hflag) {
-            *c.hflag = 0;
-            return bad_index_error();
-        }
-        std::vector<int64_t> b(2 * (kMaxGrid + 1));
-        balanced_cut(du, nnz, s, b.data());
-        balanced_cut(dv, nnz, s, b.data() + kMaxGrid + 1);
-        HIPCHK(hipMemcpy(c.bnd, b.data(), sizeof(int64_t) * b.size(), hipMemcpyHostToDevice));
+    }
+    HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(unsigned long long) * dv.size(), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    if (*c.hflag) {
+        *c.hflag = 0;
+        return bad_index_error();
+    }
+    std::vector<int64_t> cut(2 * (kMaxGrid + 1));
+    int64_t* ccut = cut.data() + kMaxGrid + 1;
+    if (balanced) {
+        balanced_cut(du, nnz, s, cut.data());
+        balanced_cut(dv, nnz, s, ccut);
+        HIPCHK(hipMemcpy(c.bnd, cut.data(), sizeof(int64_t) * cut.size(), hipMemcpyHostToDevice));
         rbnd = c.bnd;
         cbnd = c.bnd + kMaxGrid + 1;
+    } else {
+        for (int j = 0; j <= s; ++j) // first item of each equal column range floor(v*s/n) = j
+            ccut[j] = (int64_t)((j * c.n + s - 1) / s);
+    }
+    // Largest share of one column block's samples that a single item holds.
+    pl.hot_col = 0.0;
+    for (int j = 0; j < s; ++j) {
+        unsigned long long tot = 0, top = 0;
+        for (int64_t v = ccut[j]; v < ccut[j + 1]; ++v) {
+            tot += dv[(size_t)v];
+            top = std::max(top, dv[(size_t)v]);
+        }
+        if (tot > 0)
+            pl.hot_col = std::max(pl.hot_col, (double)top / (double)tot);
     }
     PlanBuffers b{c.counts, c.totals, pl.bstart, pl.Sp, keep_orig ? pl.orig : nullptr, c.bad, rbnd, cbnd};
     HIPCHK(plan_build(S, nnz, c.m, c.n, s, b, st));
@@ -656,6 +681,20 @@ int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, i
     return MFSGD_OK;
 }
 
+// Whether a block-scheduled epoch on plan pl redirects the stores of rows
+// that the same wavefront updates again within its in-flight window.
+// Automatic: when one item holds most of some column block's samples.  Every
+// team passes through that column once per epoch, so its runs of updates to
+// one row lie on the epoch's critical path; a row block dominated by one user
+// slows only its own team, and the variant's extra register pressure would
+// cost every other team more.
+bool skip_stores(const Plan& pl)
+{
+    if (g_opt.skip_stores != 2)
+        return g_opt.skip_stores != 0;
+    return pl.hot_col > 0.5;
+}
+
 // Team shape of a block-scheduled launch on plan pl with `want` wavefronts per
 // team (1: one-wavefront teams placed anywhere; 0: every co-resident slot,
 // shared in proportion to the row blocks' samples).
@@ -690,6 +729,7 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
             CHK(build_team_layout(load, nx, cap / nx, want > 0 ? (want + 3) / 4 : 0, L));
         }
         CHK(grow(&c.tmap, &c.tmap_cap, L.grid, "team map"));
+        CHK(grow(&c.sink, &c.sink_cap, L.grid * waves * 2 * c.KP * (int64_t)elem_size(c.dtype), "store sink"));
         if (!c.tsize)
             CHK(dalloc((void**)&c.tsize, sizeof(int32_t) * kMaxGrid, "team sizes"));
         HIPCHK(hipMemcpy(c.tmap, L.tmap.data(), sizeof(int32_t) * L.tmap.size(), hipMemcpyHostToDevice));
@@ -705,6 +745,7 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
     a.tmap = c.tmap;
     a.tsize = c.tsize;
     a.wg_waves = waves;
+    a.sink = skip_stores(pl) ? c.sink : nullptr;
     return MFSGD_OK;
 }
 

@@ -263,10 +263,11 @@ struct WorkerState {
     int hu[D], hv[D];
 };
 
-template <int KP, typename T, int D, bool DBG>
+template <int KP, typename T, int D, bool DBG, bool SKIP = false>
 __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t worker,
                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
-                                           float lq, const DebugSink dbg, const CacheSync sync = CacheSync{0, false, false})
+                                           float lq, const DebugSink dbg, const CacheSync sync = CacheSync{0, false, false},
+                                           T* sink = nullptr)
 {
     constexpr int E = Geo<KP>::E;
     constexpr int A = Geo<KP>::A;
@@ -358,9 +359,30 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
             q[e] = qe + lr * (err * pe - lq * qe);
         }
         const V np = R::narrow(p), nq = R::narrow(q);
+        // SKIP: a row that one of the next D-1 samples (already issued, so
+        // certain to be processed) updates again takes its value from this
+        // one by forwarding and stores it later, so this store goes to the
+        // wavefront's private sink rows instead (a select, not a branch, so
+        // the memory-counter waits stay static).  Hot rows then see one store per
+        // run of in-flight updates, and the worker's final values are
+        // unchanged.  This pays where many workers share one L2 and its hot
+        // lines (block-scheduled epochs).
+        T* pbase = P + (int64_t)u * KP;
+        T* qbase = Q + (int64_t)v * KP;
+        if constexpr (SKIP) {
+            bool p_again = false, q_again = false;
+#pragma unroll
+            for (int d = 1; d < D; ++d) {
+                const int h = (j + d) % D;
+                p_again |= st.su[h] == u;
+                q_again |= st.sv[h] == v;
+            }
+            pbase = p_again ? sink : pbase;
+            qbase = q_again ? sink + KP : qbase;
+        }
         if (holds) {
-            R::st(P + (int64_t)u * KP + col, np);
-            R::st(Q + (int64_t)v * KP + col, nq);
+            R::st(pbase + col, np);
+            R::st(qbase + col, nq);
         }
         st.hu[j] = u;
         st.hv[j] = v;

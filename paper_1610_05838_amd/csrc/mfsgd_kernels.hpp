@@ -53,13 +53,13 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 //
 // A ticket wait that exceeds spin_limit polls raises *err; every waiting
 // workgroup then leaves, so the grid always drains.
-template <int KP, typename T, int D, bool DBG>
+template <int KP, typename T, int D, bool DBG, bool SKIP>
 __global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                   int s, const int32_t* __restrict__ tmap,
                                                   const int32_t* __restrict__ tsize, uint64_t sigma_c, uint64_t sigma_o,
                                                   T* __restrict__ P, T* __restrict__ Q, float lr, float lp, float lq,
                                                   int f, uint32_t* tickets, uint32_t* done, uint32_t spin_limit,
-                                                  int* err, DebugSink dbg, int32_t* trace)
+                                                  int* err, DebugSink dbg, int32_t* trace, T* __restrict__ sink)
 {
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
     __shared__ int abort_all;
@@ -73,6 +73,8 @@ __global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp,
     const int wv = uniform(threadIdx.x >> 6);
     const int64_t W = (int64_t)G * waves;
     const int64_t worker = (int64_t)member * waves + wv;
+    // two private rows per wavefront of the grid for skipped stores
+    T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
     if (threadIdx.x == 0) {
         shuffle_perm(sigma_c, s, Cperm);
         shuffle_perm(sigma_o, s, Ooff);
@@ -113,7 +115,8 @@ __global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp,
             DebugSink blk = inner;
             if (blk.orig)
                 blk.orig += lo;
-            run_worker<KP, T, D, DBG>(Sp + lo, hi - lo, W, worker, f, P, Q, lr, lp, lq, blk);
+            run_worker<KP, T, D, DBG, SKIP>(Sp + lo, hi - lo, W, worker, f, P, Q, lr, lp, lq, blk,
+                                            CacheSync{0, false, false}, my_sink);
         }
         __syncthreads(); // every wavefront of this workgroup is done with the block
         if (threadIdx.x == 0) {
@@ -136,9 +139,14 @@ template <int KP, typename T, int D>
 static int occupancy_blocked_t(int threads)
 {
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false>, threads, 0) != hipSuccess)
+    // the co-residency cap must hold for both variants the launcher may pick
+    int plain = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false, true>, threads, 0) !=
+            hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&plain, k_blocked<KP, T, D, false, false>, threads, 0) !=
+            hipSuccess)
         return 0;
-    return blocks;
+    return blocks < plain ? blocks : plain;
 }
 
 template <int KP, typename T>
@@ -229,9 +237,15 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
                            a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
-        hipLaunchKernelGGL((k_blocked<KP, T, D, DBG>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0, st, a.S,
-                           a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f,
-                           a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave);
+        // skipped stores only in epochs without debug output (they never change results)
+        if (!DBG && a.sink)
+            hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
+                               st, a.S, a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq,
+                               a.f, a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave, (T*)a.sink);
+        else
+            hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
+                               st, a.S, a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq,
+                               a.f, a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr);
     }
     return hipGetLastError();
 }

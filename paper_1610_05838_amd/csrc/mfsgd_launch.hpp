@@ -37,6 +37,7 @@ struct EpochLaunch {
     const int32_t* tmap;  // per workgroup: team << 16 | member, or -1 (idle)
     const int32_t* tsize; // per team: its workgroup count
     int wg_waves;    // wavefronts per workgroup
+    void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
     uint64_t sigma_c, sigma_o;
     uint32_t* tickets;
     uint32_t* done;  // arrival counters, one per (team, wave): s*s entries

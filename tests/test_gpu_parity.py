@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 
 TOL = {np.float32: 1e-4, np.float16: 2e-2}
 DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=4, team_waves=0, partition=2, hogwild_grid=0, balance=1,
-                sync_every=0, sync_l1=0, spin_limit=1 << 24, debug=0)
+                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0)
 
 
 @pytest.fixture(scope="module")
@@ -254,14 +254,15 @@ def test_wavefront_schedule_and_coverage(M, scheme):
 
 
 # ---------------------------------------------------------------------------- deterministic wavefront
+@pytest.mark.parametrize("skip", [0, 1])
 @pytest.mark.parametrize("balance", [0, 1])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 @pytest.mark.parametrize("s", [1, 3, 8, 32])
-def test_wavefront_det_matches_oracle(M, gen, dtype, s, balance):
+def test_wavefront_det_matches_oracle(M, gen, dtype, s, balance, skip):
     w = gen.workload("tiny")
     S, _ = gen.make(w)
     m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
-    setup(M, m, n, k, seed, dtype, balance=balance)
+    setup(M, m, n, k, seed, dtype, balance=balance, skip_stores=skip)
     dS = M.samples_to_device(S)
     M.plan(dS, s)
     Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
@@ -272,11 +273,14 @@ def test_wavefront_det_matches_oracle(M, gen, dtype, s, balance):
     assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
 
-def test_wavefront_det_k128_zipf(M, gen):
+@pytest.mark.parametrize("skip", [0, 1])
+def test_wavefront_det_k128_zipf(M, gen, skip):
+    """Zipf-skewed indices: runs of one hot row inside a block, where skipped
+    stores (skip=1) must leave the final values unchanged."""
     w = gen.workload("netflix", m=20_000, n=3_000, ntrain=400_000, ntest=0)
     S = gen.draw(w, 0, w["ntrain"])
     m, n, k, seed, s = w["m"], w["n"], w["k"], w["seed"], 16
-    setup(M, m, n, k, seed)
+    setup(M, m, n, k, seed, skip_stores=skip)
     dS = M.samples_to_device(S)
     M.plan(dS, s)
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
