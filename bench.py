@@ -44,15 +44,16 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel_key: str):
+def measured_traffic(kernel_key: str, variant: list):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources; else None."""
+    was taken on the current kernel sources with the same bench options
+    (`variant`: the options that change the launch); else None."""
     path = os.path.join(PROFILE_DIR, f"traffic_{kernel_key}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    if d.get("source_digest") != source_digest():
+    if d.get("source_digest") != source_digest() or d.get("bench_args", []) != variant:
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -211,7 +212,10 @@ def main():
     achieved_gbs = nnz * bytes_per_update / avg_epoch_s / 1e9
     value = nnz * args.steps / wall
     key = f"{kernel}_{args.scheme}_{w['name']}"
-    traffic = measured_traffic(key)
+    variant = [x for x in sys.argv[1:] if x not in ("--no-cpu-baseline", "--copy-calibration")]
+    drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus"}
+    variant = [x for i, x in enumerate(variant) if x not in drop and (i == 0 or variant[i - 1] not in drop)]
+    traffic = measured_traffic(key, variant)
     out = {
         "metric": "SGD updates/sec and achieved HBM GB/s (% of peak) at k=128, 1 MI355X",
         "value": value,
