@@ -121,6 +121,8 @@ def main():
     ap.add_argument("--team-waves", type=int, default=0)
     ap.add_argument("--partition", type=int, default=2, help="batch-Hogwild!: 0 one address space, 1 XCD-partitioned, 2 automatic")
     ap.add_argument("--ntrain", type=int, default=0, help="override the training size (0: the workload's)")
+    ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
+                    help="further library option (mfsgd_set_option), applied before init")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -163,6 +165,9 @@ def main():
     for key, val in dict(dtype=dtype, batch_f=256, workers=args.workers, depth=args.depth,
                          team_waves=args.team_waves, partition=args.partition, debug=0).items():
         mfsgd.set_option(key, val)
+    for kv in args.set:
+        key, val = kv.split("=", 1)
+        mfsgd.set_option(key, int(val))
     mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
     resident = mfsgd.get_option("resident_waves")
     partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1

@@ -70,7 +70,7 @@ struct Context {
     void* P = nullptr;
     void* Q = nullptr;
     uint32_t* tickets = nullptr;
-    uint32_t* done = nullptr;
+    uint32_t* sched = nullptr; // block-scheduled claim state (kSchedWords)
     int* err = nullptr;
     int* bad = nullptr;
     double* partial = nullptr;
@@ -94,6 +94,7 @@ struct Context {
     int32_t* tmap = nullptr;
     int64_t tmap_cap = 0;
     int32_t* tsize = nullptr;
+    int32_t* xteams = nullptr; // kMaxGrid * (kMaxGrid + 1): per XCD, team count then teams
     unsigned char* sink = nullptr; // rows for skipped stores, 2 per wavefront of the grid
     int64_t sink_cap = 0;
     const Plan* lay_plan = nullptr;
@@ -187,7 +188,7 @@ void release_all()
     dfree(c.P);
     dfree(c.Q);
     dfree(c.tickets);
-    dfree(c.done);
+    dfree(c.sched);
     dfree(c.err);
     dfree(c.bad);
     dfree(c.partial);
@@ -206,6 +207,7 @@ void release_all()
     dfree(c.trace);
     dfree(c.tmap);
     dfree(c.tsize);
+    dfree(c.xteams);
     dfree(c.sink);
     c = Context();
 }
@@ -396,7 +398,7 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     int rc;
     if ((rc = dalloc(&c.P, (size_t)m * c.KP * es, "P")) || (rc = dalloc(&c.Q, (size_t)n * c.KP * es, "Q")) ||
         (rc = dalloc((void**)&c.tickets, sizeof(uint32_t) * kMaxGrid, "tickets")) ||
-        (rc = dalloc((void**)&c.done, sizeof(uint32_t) * kMaxGrid * kMaxGrid, "team counters")) ||
+        (rc = dalloc((void**)&c.sched, sizeof(uint32_t) * kSchedWords, "claim counters")) ||
         (rc = dalloc((void**)&c.err, sizeof(int), "flag")) || (rc = dalloc((void**)&c.bad, sizeof(int), "flag")) ||
         (rc = dalloc((void**)&c.partial, sizeof(double) * kRmseWaves, "rmse partials")) ||
         (rc = dalloc((void**)&c.dres, sizeof(double), "rmse result")) ||
@@ -413,7 +415,7 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     *c.hflag = 0;
     HIPCHK(hipMemset(c.err, 0, sizeof(int)));
     HIPCHK(hipMemset(c.bad, 0, sizeof(int)));
-    HIPCHK(reset_tickets(c.tickets, c.done, nullptr));
+    HIPCHK(reset_tickets(c.tickets, c.sched, nullptr));
     const double inv_sqrt_k = 1.0 / std::sqrt((double)k);
     const uint64_t sp = sm64_at(seed, kTagP), sq = sm64_at(seed, kTagQ);
     if (c.dtype == MFSGD_FP16) {
@@ -609,6 +611,7 @@ int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
 // Slot j of XCD x is workgroup j * nx + x (round-robin dispatch).
 struct TeamLayout {
     std::vector<int32_t> tmap, tsize;
+    std::vector<int32_t> xteams; // per XCD: team count, then the teams placed there
     int64_t grid = 0;
 };
 
@@ -665,6 +668,11 @@ int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, i
                 L.tsize[rem[i].second] += 1;
         }
     }
+    L.xteams.assign((size_t)nx * (kMaxGrid + 1), 0);
+    for (int t = 0; t < s; ++t) {
+        int32_t* xt = &L.xteams[(size_t)xcd[t] * (kMaxGrid + 1)];
+        xt[1 + xt[0]++] = t;
+    }
     std::vector<int64_t> fill(nx, 0);
     for (int t = 0; t < s; ++t)
         fill[xcd[t]] += L.tsize[t];
@@ -696,13 +704,16 @@ bool skip_stores(const Plan& pl)
 }
 
 // Team shape of a block-scheduled launch on plan pl with `want` wavefronts per
-// team (1: one-wavefront teams placed anywhere; 0: every co-resident slot,
-// shared in proportion to the row blocks' samples).
+// team (1: one-wavefront teams placed anywhere, each serving only its own
+// team; 0: every workgroup slot the occupancy allows, home teams shared in
+// proportion to the row blocks' samples, every wavefront also serving the
+// other teams of its XCD).
 int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
 {
     Context& c = g;
     const int s = pl.s;
     const int waves = want == 1 ? 1 : 4;
+    const int nx = std::max(1, c.nx);
     if (c.lay_plan != &pl || c.lay_version != pl.version || c.lay_want != want || c.lay_waves != waves ||
         c.lay_depth != a.depth) {
         TeamLayout L;
@@ -712,17 +723,16 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
             L.tmap.resize(s);
             for (int t = 0; t < s; ++t)
                 L.tmap[t] = t << 16;
+            L.xteams.assign((size_t)nx * (kMaxGrid + 1), 0);
         } else {
             const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 64 * waves);
             if (per_cu <= 0)
                 return fail(MFSGD_EHIP, "occupancy query failed for the block-scheduled kernel");
-            // Every workgroup of this persistent grid must be resident at once
-            // (teams wait on each other).  Measured on MI355X, fewer workgroups
-            // fit than the occupancy query reports (about 5.3 of 7 per CU), so
-            // only half of the reported count is used.  A grid that still did
-            // not fit would end in MFSGD_ETIMEOUT, not a hang.
-            const int64_t cap = (int64_t)std::max(1, per_cu / 2) * c.cus;
-            const int nx = std::max(1, c.nx);
+            // Work is claimed, not assigned, so no workgroup has to be
+            // resident for the others to progress (one per XCD is enough, and
+            // the first nx workgroups of the grid are on distinct XCDs): the
+            // grid takes every slot the occupancy query reports.
+            const int64_t cap = (int64_t)per_cu * c.cus;
             std::vector<int64_t> load(s);
             for (int t = 0; t < s; ++t)
                 load[t] = pl.hstart[(size_t)(t + 1) * s] - pl.hstart[(size_t)t * s];
@@ -732,7 +742,10 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
         CHK(grow(&c.sink, &c.sink_cap, L.grid * waves * 2 * c.KP * (int64_t)elem_size(c.dtype), "store sink"));
         if (!c.tsize)
             CHK(dalloc((void**)&c.tsize, sizeof(int32_t) * kMaxGrid, "team sizes"));
+        if (!c.xteams)
+            CHK(dalloc((void**)&c.xteams, sizeof(int32_t) * kMaxGrid * (kMaxGrid + 1), "XCD team lists"));
         HIPCHK(hipMemcpy(c.tmap, L.tmap.data(), sizeof(int32_t) * L.tmap.size(), hipMemcpyHostToDevice));
+        HIPCHK(hipMemcpy(c.xteams, L.xteams.data(), sizeof(int32_t) * L.xteams.size(), hipMemcpyHostToDevice));
         HIPCHK(hipMemcpy(c.tsize, L.tsize.data(), sizeof(int32_t) * L.tsize.size(), hipMemcpyHostToDevice));
         c.lay_plan = &pl;
         c.lay_version = pl.version;
@@ -743,7 +756,9 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
     }
     a.grid = c.lay_grid;
     a.tmap = c.tmap;
-    a.tsize = c.tsize;
+    a.xteams = c.xteams;
+    a.nx = nx;
+    a.pool = want == 1 ? 0 : 1;
     a.wg_waves = waves;
     a.sink = skip_stores(pl) ? c.sink : nullptr;
     return MFSGD_OK;
@@ -843,7 +858,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;
-        a.done = c.done;
+        a.sched = c.sched;
         a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
             CHK(grow(&c.trace, &c.trace_cap, (int64_t)s * s, "trace"));
@@ -851,7 +866,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)s * s, st));
             a.trace_wave = c.trace;
         }
-        HIPCHK(reset_tickets(c.tickets, c.done, st));
+        HIPCHK(reset_tickets(c.tickets, c.sched, st));
         if (c.dtype == MFSGD_FP16)
             HIPCHK(epoch_f16(a, st));
         else

@@ -55,18 +55,18 @@ hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int
     return hipGetLastError();
 }
 
-__global__ void k_reset_tickets(uint32_t* tickets, uint32_t* done)
+__global__ void k_reset_tickets(uint32_t* tickets, uint32_t* sched)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < kMaxGrid)
         tickets[i] = 0u;
-    if (i < kMaxGrid * kMaxGrid)
-        done[i] = 0u;
+    if (i < kSchedWords)
+        sched[i] = 0u;
 }
 
-hipError_t reset_tickets(uint32_t* tickets, uint32_t* done, hipStream_t st)
+hipError_t reset_tickets(uint32_t* tickets, uint32_t* sched, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_reset_tickets, dim3(kMaxGrid * kMaxGrid / 256), dim3(256), 0, st, tickets, done);
+    hipLaunchKernelGGL(k_reset_tickets, dim3((kSchedWords + 255) / 256), dim3(256), 0, st, tickets, sched);
     return hipGetLastError();
 }
 

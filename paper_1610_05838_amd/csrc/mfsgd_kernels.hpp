@@ -31,106 +31,160 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 // Block-scheduled epoch: wavefront-update (section 3.2.3), and
 // batch-Hogwild! partitioned over the GPU's coherence domains.
 //
-// The s x s grid of blocks is processed in s waves.  Worker (team) i owns row
-// block i and in wave w takes column block sigma_i(w) = C[(i + O[w]) mod s],
-// so the blocks of one wave share no row and no column.  Column tickets order
-// the waves: team i starts wave w once ticket[sigma_i(w)] reads w, and the
-// last member to finish releases it with w+1 (every column is used by exactly
-// one team per wave, so a ticket counts the waves completed on its column).
+// The s x s grid of blocks is processed in s waves.  Team (row block) t in
+// wave w works on column block sigma_t(w) = C[(t + O[w]) mod s], so the blocks
+// of one wave share no row and no column.  A column ticket counts the waves
+// completed on its column: block (t, w) opens once ticket[sigma_t(w)] has
+// reached w, and the wavefront that finishes the block's last batch sets it to
+// w + 1 (each column is used by exactly one team per wave).
 //
-// A team is a set of workgroups; inside a block its wavefronts run
-// batch-Hogwild! (run_worker) over the block's samples.  Members do not wait
-// for each other between waves (they share the team's row block, which no
-// other team touches); the last one to finish a wave releases its column.
-// tmap[b] gives the team and member index of workgroup b (-1: idle), tsize[i]
-// the workgroup count of team i.  The host builds the map so that every
-// member of a team sits on one XCD (workgroup b runs on XCD b mod nx, checked
-// at init) and teams get workgroups in proportion to their row block's
-// samples; the team's unsynchronised updates then meet in that XCD's shared
-// L2.  Feature rows move between teams only at block hand-over, through an
-// agent-scope release (L2 write-back) and acquire (L1/L2 invalidate),
-// whichever XCDs the two teams run on.
+// Inside an open block the batches of f consecutive samples are claimed one
+// at a time from the block's claim counter, and each is run serially by one
+// wavefront (run_worker); concurrent batches of a block race as in
+// batch-Hogwild!.  A team's teams-mates may already work on the team's next
+// block while the last batches of the previous one run (the two share only
+// the team's row block).  cursor[t] is the lowest wave of team t that may still
+// have unclaimed batches.
 //
-// A ticket wait that exceeds spin_limit polls raises *err; every waiting
-// workgroup then leaves, so the grid always drains.
+// Every team lives on one XCD (workgroup b runs on XCD b mod nx, checked at
+// init), so all updates of a team meet in that XCD's L2.  In pool mode a
+// wavefront serves its home team first and otherwise any open block of the
+// other teams on its XCD; without pool mode (one-wavefront teams: the
+// deterministic schedule) only its home team.  Rows move between XCDs only
+// at block hand-over: the releasing wavefront writes its XCD's L2 back
+// (agent-scope release) before it advances the ticket, and a wavefront
+// entering a block invalidates its caches (agent-scope acquire) first.
+//
+// Nothing waits for a particular workgroup: work is claimed, not assigned,
+// so workgroups that become resident late (or never, before the others
+// finish) are harmless, and the grid may be as large as the occupancy allows.
+// A wait for an open block that exceeds spin_limit polls raises *err; every
+// wavefront that then finds nothing to claim leaves, so the grid drains.
+//
+// sched: [0, G2) batches finished per (team, wave), [G2, 2 G2) next batch to
+// claim per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, where
+// G2 = kMaxGrid^2; all zero at launch.
 template <int KP, typename T, int D, bool DBG, bool SKIP>
-__global__ __launch_bounds__(1024) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
-                                                  int s, const int32_t* __restrict__ tmap,
-                                                  const int32_t* __restrict__ tsize, uint64_t sigma_c, uint64_t sigma_o,
-                                                  T* __restrict__ P, T* __restrict__ Q, float lr, float lp, float lq,
-                                                  int f, uint32_t* tickets, uint32_t* done, uint32_t spin_limit,
-                                                  int* err, DebugSink dbg, int32_t* trace, T* __restrict__ sink)
+__global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
+                                                 int s, const int32_t* __restrict__ tmap,
+                                                 const int32_t* __restrict__ xteams, int nx, int pool,
+                                                 uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
+                                                 T* __restrict__ Q, float lr, float lp, float lq, int f,
+                                                 uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
+                                                 DebugSink dbg, int32_t* trace, T* __restrict__ sink)
 {
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
-    __shared__ int abort_all;
     const int tm = tmap[blockIdx.x];
     if (tm < 0)
         return;
-    const int team = tm >> 16;
-    const int member = tm & 0xffff;
-    const int G = tsize[team];
+    const int home = tm >> 16;
+    const int lane = lane_id();
     const int waves = blockDim.x >> 6;
     const int wv = uniform(threadIdx.x >> 6);
-    const int64_t W = (int64_t)G * waves;
-    const int64_t worker = (int64_t)member * waves + wv;
+    uint32_t* const fin = sched;
+    uint32_t* const claim = sched + kMaxGrid * kMaxGrid;
+    uint32_t* const cursor = sched + 2 * kMaxGrid * kMaxGrid;
     // two private rows per wavefront of the grid for skipped stores
     T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
     if (threadIdx.x == 0) {
         shuffle_perm(sigma_c, s, Cperm);
         shuffle_perm(sigma_o, s, Ooff);
-        abort_all = 0;
     }
     __syncthreads();
-    DebugSink inner = dbg;
-    inner.trace = nullptr;
-    for (int w = 0; w < s; ++w) {
-        const int col = Cperm[(team + Ooff[w]) % s];
-        if (threadIdx.x == 0) {
-            // Poll with an atomic read-modify-write: it is resolved at the
-            // device's coherence point, whereas a plain (even agent-scope) load
-            // may keep hitting a stale copy in this XCD's L2.  Acquire once the
-            // ticket has come round, which invalidates this CU's L1 and this
-            // XCD's L2 before the block's rows are read.
-            uint32_t polls = 0;
-            while (__hip_atomic_fetch_or(tickets + col, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) !=
-                   (uint32_t)w) {
-                if (++polls > spin_limit ||
-                    __hip_atomic_fetch_or(err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+
+    // lane j < nt watches the j-th team of this wavefront's preference order:
+    // the home team, then the other teams of the XCD in list order
+    const int32_t* xt = xteams + (int64_t)(blockIdx.x % nx) * (kMaxGrid + 1);
+    const int nt = pool ? xt[0] : 1;
+    int hidx = 0;
+    for (int j = 0; pool && j < nt; ++j)
+        hidx = xt[1 + j] == home ? j : hidx;
+    const int lt = lane < nt ? (pool ? xt[1 + (hidx + lane) % nt] : home) : -1;
+
+    int64_t entered = -1; // (team, wave) whose data this wavefront has acquired
+    uint32_t polls = 0;
+    for (;;) {
+        int cw = s;
+        bool open = false;
+        if (lt >= 0) {
+            cw = (int)__hip_atomic_load(cursor + lt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (cw < s) {
+                const int col = Cperm[(lt + Ooff[cw]) % s];
+                open = __hip_atomic_load(tickets + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= (uint32_t)cw;
+            }
+        }
+        if (__builtin_amdgcn_ballot_w64(cw < s) == 0)
+            return; // every batch of every watched team has been claimed
+        const uint64_t avail = __builtin_amdgcn_ballot_w64(open);
+        if (avail == 0) {
+            int stop = 0;
+            if (lane == 0)
+                stop = ++polls > spin_limit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__builtin_amdgcn_readfirstlane(stop)) {
+                if (lane == 0)
                     __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    abort_all = 1;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(4);
+                return;
             }
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            if (trace && member == 0)
-                trace[(int64_t)team * s + w] = col;
+            __builtin_amdgcn_s_sleep(4);
+            continue;
         }
-        __syncthreads();
-        if (abort_all)
-            return;
-        const int64_t b = (int64_t)team * s + col;
+        polls = 0;
+        const int j = (int)__builtin_ctzll(avail);
+        const int t = __builtin_amdgcn_readlane(lt, j);
+        const int w = __builtin_amdgcn_readlane(cw, j);
+        const int col = Cperm[(t + Ooff[w]) % s];
+        const int64_t tw = (int64_t)t * s + w;
+        const int64_t b = (int64_t)t * s + col;
         const int64_t lo = bstart[b], hi = bstart[b + 1];
-        if (hi > lo) {
-            DebugSink blk = inner;
-            if (blk.orig)
-                blk.orig += lo;
-            run_worker<KP, T, D, DBG, SKIP>(Sp + lo, hi - lo, W, worker, f, P, Q, lr, lp, lq, blk,
-                                            CacheSync{0, false, false}, my_sink);
-        }
-        __syncthreads(); // every wavefront of this workgroup is done with the block
-        if (threadIdx.x == 0) {
-            if (G == 1) {
-                __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-            } else {
-                // one counter per (team, wave): a member may already be in the
-                // next wave (its next column can come free first) while another
-                // is still finishing this one
-                const uint32_t before = __hip_atomic_fetch_add(done + (int64_t)team * s + w, 1u, __ATOMIC_ACQ_REL,
-                                                               __HIP_MEMORY_SCOPE_AGENT);
-                if (before == (uint32_t)(G - 1)) // last member of the team to finish this wave
+        const uint32_t nb = (uint32_t)((hi - lo + f - 1) / f);
+        uint32_t idx = 0;
+        if (lane == 0)
+            idx = __hip_atomic_fetch_add(claim + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        idx = __builtin_amdgcn_readfirstlane(idx);
+        if (idx >= nb) {
+            // nothing left to claim in this block: move the team's cursor on;
+            // an empty block is released by its only claimant
+            if (lane == 0) {
+                if (nb == 0 && idx == 0) {
+                    if (trace)
+                        trace[tw] = col;
                     __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                uint32_t expect = (uint32_t)w;
+                __hip_atomic_compare_exchange_strong(cursor + t, &expect, (uint32_t)(w + 1), __ATOMIC_RELAXED,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            continue;
+        }
+        if (trace && idx == 0 && lane == 0)
+            trace[tw] = col;
+        if (entered != tw) {
+            // the ticket was read before: rows of this block written on other
+            // XCDs become visible once this wavefront's caches are invalidated
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            entered = tw;
+        }
+        const int64_t b0 = lo + (int64_t)idx * f;
+        const int64_t cnt = hi - b0 < f ? hi - b0 : f;
+        DebugSink blk = dbg;
+        blk.trace = nullptr;
+        if (blk.orig)
+            blk.orig += b0;
+        run_worker<KP, T, D, DBG, SKIP>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk, CacheSync{0, false, false},
+                                        my_sink);
+        // this wavefront's stores have reached the XCD's L2 before it counts
+        // the batch as finished
+        __builtin_amdgcn_s_waitcnt(0);
+        uint32_t done = 0;
+        if (lane == 0)
+            done = __hip_atomic_fetch_add(fin + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        done = __builtin_amdgcn_readfirstlane(done);
+        if (done == nb - 1) {
+            // last batch of the block: every batch's stores are in this XCD's
+            // L2; write it back, then pass the column on
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            if (lane == 0)
+                __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -240,12 +294,14 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq,
-                               a.f, a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave, (T*)a.sink);
+                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.sigma_c, a.sigma_o, P, Q,
+                               a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
+                               (T*)a.sink);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.tsize, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq,
-                               a.f, a.tickets, a.done, a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr);
+                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.sigma_c, a.sigma_o, P, Q,
+                               a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
+                               (T*)nullptr);
     }
     return hipGetLastError();
 }

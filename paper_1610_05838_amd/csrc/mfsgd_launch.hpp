@@ -13,6 +13,8 @@ constexpr int kMaxGrid = 64;      // largest wavefront-update grid side s
 constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never changes
 constexpr int kSchemeHogwild = 0;
 constexpr int kSchemeWavefront = 1;
+// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team
+constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid;
 
 struct DebugSink;
 
@@ -34,13 +36,14 @@ struct EpochLaunch {
     const int64_t* bstart;
     int s;           // grid side
     int grid;        // workgroups launched
-    const int32_t* tmap;  // per workgroup: team << 16 | member, or -1 (idle)
-    const int32_t* tsize; // per team: its workgroup count
+    const int32_t* tmap;   // per workgroup: home team << 16 | member, or -1 (idle)
+    const int32_t* xteams; // per XCD x: [x * (kMaxGrid + 1)] = team count, then the teams placed on x
+    int pool;              // 1: a wavefront also serves the other teams of its XCD
     int wg_waves;    // wavefronts per workgroup
     void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
     uint64_t sigma_c, sigma_o;
     uint32_t* tickets;
-    uint32_t* done;  // arrival counters, one per (team, wave): s*s entries
+    uint32_t* sched; // claim state, kSchedWords entries (see k_blocked)
     uint32_t spin_limit;
     int* err;
     int32_t* trace_wave;
@@ -67,8 +70,8 @@ hipError_t init_f16(void* A, int64_t rows, int k, int KP, uint64_t stream, doubl
 // Implemented in mfsgd_aux.hip (type-independent kernels).
 hipError_t rmse_final(const double* partial, int64_t ntest, double* out, hipStream_t st);
 hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int* bad, hipStream_t st);
-// zero the column tickets and the kMaxGrid^2 arrival counters (a fill kernel, safe under graph capture)
-hipError_t reset_tickets(uint32_t* tickets, uint32_t* done, hipStream_t st);
+// zero the column tickets and the kSchedWords claim counters (a fill kernel, safe under graph capture)
+hipError_t reset_tickets(uint32_t* tickets, uint32_t* sched, hipStream_t st);
 // XCC id of each of `n` one-wavefront workgroups (to learn the dispatch layout)
 hipError_t probe_xcc(int* out, int n, hipStream_t st);
 // stable bucketing of samples into the s x s grid
