@@ -122,11 +122,16 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  epoch as diverging copies), one address space above that.
  *   "hogwild_grid" grid side of the partitioned batch-Hogwild!; 0 (default)
  *                  = number of XCDs.
- *   "balance"      how a grid is cut: 1 (default) into consecutive index
- *                  ranges holding as equal sample counts as consecutive
- *                  ranges allow (the smallest possible largest range, ranges
+ *   "balance"      how a grid is cut: 1 into consecutive index ranges
+ *                  holding as equal sample counts as consecutive ranges
+ *                  allow (the smallest possible largest range, ranges
  *                  filled greedily at that size); 0 into equal index ranges
- *                  floor(u*s/m), floor(v*s/n).
+ *                  floor(u*s/m), floor(v*s/n); 2 (default) automatic: 1
+ *                  when s is at most the number of XCDs (each worker then
+ *                  has an XCD to itself, so the largest row block sets the
+ *                  epoch time), 0 above (the workers sharing an XCD share
+ *                  its wavefronts, and the greedy fill can leave ranges
+ *                  empty when one index holds a large share).
  *   "sync_every"   one-address-space batch-Hogwild!: every this many of its
  *                  batches, one wavefront per XCD writes that XCD's L2 back
  *                  and invalidates it, bounding how long an update stays
@@ -138,10 +143,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *   "skip_stores"  block-scheduled epochs: a wavefront that updates a row
  *                  again within its in-flight window writes it back once per
  *                  run (the final values are the same).  0 never, 1 always,
- *                  2 (default) when one item holds more than half of the
- *                  samples of its column block (every worker passes through
- *                  that column each epoch).  Epochs with debug output never
- *                  skip.
+ *                  2 (default) when one user or one item holds more than
+ *                  half of the samples of its row or column block (many
+ *                  wavefronts then update one row at once).  Epochs with
+ *                  debug output never skip.
  *   "debug"        bit 0: count visits of every sample (read with
  *                  mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
  *                  schedule (MFSGD_DBG_TRACE).  Costs one extra atomic per

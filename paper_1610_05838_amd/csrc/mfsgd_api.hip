@@ -26,7 +26,7 @@ struct Options {
     int64_t team_waves = 0;
     int64_t partition = 2;
     int64_t hogwild_grid = 0;
-    int64_t balance = 1;
+    int64_t balance = 2;
     int64_t sync_every = 0;
     int64_t sync_l1 = 0;
     int64_t spin_limit = int64_t(1) << 24;
@@ -48,6 +48,7 @@ struct Plan {
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
     double hot_col = 0.0;        // largest share of a column block's samples held by one item
+    double hot_row = 0.0;        // largest share of a row block's samples held by one user
     uint64_t version = 0;        // bumped by every build
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
     bool valid() const { return nnz >= 0 && bstart != nullptr; }
@@ -293,7 +294,7 @@ const OptSpec kOpts[] = {
     {"team_waves", &Options::team_waves, 0, 65536, "team_waves must be in [0, 65536]"},
     {"partition", &Options::partition, 0, 2, "partition must be 0, 1 or 2"},
     {"hogwild_grid", &Options::hogwild_grid, 0, kMaxGrid, "hogwild_grid must be in [0, 64]"},
-    {"balance", &Options::balance, 0, 1, "balance must be 0 or 1"},
+    {"balance", &Options::balance, 0, 2, "balance must be 0, 1 or 2"},
     {"sync_every", &Options::sync_every, 0, int64_t(1) << 30, "sync_every must be in [0, 2^30]"},
     {"sync_l1", &Options::sync_l1, 0, 1, "sync_l1 must be 0 or 1"},
     {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
@@ -487,6 +488,13 @@ void balanced_cut(const std::vector<unsigned long long>& cnt, int64_t nnz, int s
     greedy_ranges(pre, lo, s, bounds);
 }
 
+// Whether an s x s grid is cut by sample counts (option "balance"; automatic:
+// when no XCD hosts two of its workers).
+bool balanced_grid(int s)
+{
+    return g_opt.balance == 1 || (g_opt.balance == 2 && s <= std::max(1, g.nx));
+}
+
 int bad_index_error()
 {
     return fail(MFSGD_EINVAL, "a sample index is out of range (need 0 <= u < m and 0 <= v < n)");
@@ -510,16 +518,13 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
     const int64_t* rbnd = nullptr;
     const int64_t* cbnd = nullptr;
-    // per-index sample counts: the balanced cut needs both, the hot-column
-    // measure below the items'
+    // per-index sample counts: the balanced cut and the hot-row and
+    // hot-column measures below need both
     CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
     HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
     HIPCHK(plan_degrees(S, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
-    std::vector<unsigned long long> du, dv((size_t)c.n);
-    if (balanced) {
-        du.resize((size_t)c.m);
-        HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(unsigned long long) * du.size(), hipMemcpyDeviceToHost, st));
-    }
+    std::vector<unsigned long long> du((size_t)c.m), dv((size_t)c.n);
+    HIPCHK(hipMemcpyAsync(du.data(), c.deg, sizeof(unsigned long long) * du.size(), hipMemcpyDeviceToHost, st));
     HIPCHK(hipMemcpyAsync(dv.data(), c.deg + c.m, sizeof(unsigned long long) * dv.size(), hipMemcpyDeviceToHost, st));
     HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
     HIPCHK(hipStreamSynchronize(st));
@@ -536,20 +541,28 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
         rbnd = c.bnd;
         cbnd = c.bnd + kMaxGrid + 1;
     } else {
-        for (int j = 0; j <= s; ++j) // first item of each equal column range floor(v*s/n) = j
+        for (int j = 0; j <= s; ++j) { // first index of each equal range floor(x*s/N) = j
+            cut[j] = (int64_t)((j * c.m + s - 1) / s);
             ccut[j] = (int64_t)((j * c.n + s - 1) / s);
-    }
-    // Largest share of one column block's samples that a single item holds.
-    pl.hot_col = 0.0;
-    for (int j = 0; j < s; ++j) {
-        unsigned long long tot = 0, top = 0;
-        for (int64_t v = ccut[j]; v < ccut[j + 1]; ++v) {
-            tot += dv[(size_t)v];
-            top = std::max(top, dv[(size_t)v]);
         }
-        if (tot > 0)
-            pl.hot_col = std::max(pl.hot_col, (double)top / (double)tot);
     }
+    // Largest share of one block row's (column's) samples that a single user
+    // (item) holds.
+    auto hottest = [s](const std::vector<unsigned long long>& d, const int64_t* bnd) {
+        double h = 0.0;
+        for (int j = 0; j < s; ++j) {
+            unsigned long long tot = 0, top = 0;
+            for (int64_t x = bnd[j]; x < bnd[j + 1]; ++x) {
+                tot += d[(size_t)x];
+                top = std::max(top, d[(size_t)x]);
+            }
+            if (tot > 0)
+                h = std::max(h, (double)top / (double)tot);
+        }
+        return h;
+    };
+    pl.hot_row = hottest(du, cut.data());
+    pl.hot_col = hottest(dv, ccut);
     PlanBuffers b{c.counts, c.totals, pl.bstart, pl.Sp, keep_orig ? pl.orig : nullptr, c.bad, rbnd, cbnd};
     HIPCHK(plan_build(S, nnz, c.m, c.n, s, b, st));
     HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
@@ -580,7 +593,7 @@ int plan_impl(const mfsgd_sample* samples, int64_t nnz, int32_t s, hipStream_t s
         return fail(MFSGD_EINVAL, "bad sample array");
     if (s < 1 || s > kMaxGrid)
         return fail(MFSGD_EINVAL, "grid side s must be in [1, 64]");
-    return build_plan(g.wf, samples, nnz, s, g_opt.balance != 0, (g_opt.debug & 1) != 0, st);
+    return build_plan(g.wf, samples, nnz, s, balanced_grid(s), (g_opt.debug & 1) != 0, st);
 }
 
 int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
@@ -691,16 +704,16 @@ int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, i
 
 // Whether a block-scheduled epoch on plan pl redirects the stores of rows
 // that the same wavefront updates again within its in-flight window.
-// Automatic: when one item holds most of some column block's samples.  Every
-// team passes through that column once per epoch, so its runs of updates to
-// one row lie on the epoch's critical path; a row block dominated by one user
-// slows only its own team, and the variant's extra register pressure would
-// cost every other team more.
+// Automatic: when one user or one item holds most of some row or column
+// block's samples.  Many wavefronts then work on the same row at once (a
+// hot row block's batches are claimed concurrently; every team passes
+// through a hot column), and its L2 lines become the bottleneck; otherwise
+// the variant's extra register pressure costs more than it saves.
 bool skip_stores(const Plan& pl)
 {
     if (g_opt.skip_stores != 2)
         return g_opt.skip_stores != 0;
-    return pl.hot_col > 0.5;
+    return pl.hot_col > 0.5 || pl.hot_row > 0.5;
 }
 
 // Team shape of a block-scheduled launch on plan pl with `want` wavefronts per
@@ -787,9 +800,9 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
     } else if (blocked) {
         const int s_h = g_opt.hogwild_grid > 0 ? (int)g_opt.hogwild_grid : c.nx;
         const bool keep = (dbg & 1) != 0;
-        if (!c.hw.matches(samples, nnz) || c.hw.s != s_h || c.hw.balanced != (g_opt.balance != 0) ||
+        if (!c.hw.matches(samples, nnz) || c.hw.s != s_h || c.hw.balanced != balanced_grid(s_h) ||
             (keep && !c.hw.has_orig))
-            CHK(build_plan(c.hw, samples, nnz, s_h, g_opt.balance != 0, keep, st));
+            CHK(build_plan(c.hw, samples, nnz, s_h, balanced_grid(s_h), keep, st));
         pl = &c.hw;
     }
     if (blocked && (dbg & 1) && !pl->has_orig)
