@@ -119,7 +119,13 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
  *                  partitioned when P and Q together take at most 64 MiB
  *                  (they would otherwise sit in every XCD's L2 for the whole
- *                  epoch as diverging copies), one address space above that.
+ *                  epoch as diverging copies), one address space above that;
+ *                  3 partitioned without the column tickets: each worker
+ *                  walks its column blocks in its wavefront order without
+ *                  waiting, so workers that drift apart may share a column
+ *                  block, whose rows are then updated on two XCDs at once as
+ *                  in one address space (the fastest form; it converges per
+ *                  epoch like 1).
  *   "hogwild_grid" grid side of the partitioned batch-Hogwild!; 0 (default)
  *                  = number of XCDs.
  *   "balance"      how a grid is cut: 1 into consecutive index ranges

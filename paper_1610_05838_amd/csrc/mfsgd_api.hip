@@ -271,7 +271,7 @@ constexpr int64_t kPartitionBytes = int64_t(64) << 20;
 bool partitioned_hogwild()
 {
     if (g_opt.partition != 2)
-        return g_opt.partition == 1;
+        return g_opt.partition == 1 || g_opt.partition == 3;
     const int64_t model = (g.m + g.n) * (int64_t)g.KP * (int64_t)elem_size(g.dtype);
     return model <= kPartitionBytes;
 }
@@ -292,7 +292,7 @@ const OptSpec kOpts[] = {
     {"workers", &Options::workers, 0, int64_t(1) << 30, "workers must be in [0, 2^30]"},
     {"depth", &Options::depth, 1, 8, "depth must be 1, 2, 4 or 8"},
     {"team_waves", &Options::team_waves, 0, 65536, "team_waves must be in [0, 65536]"},
-    {"partition", &Options::partition, 0, 2, "partition must be 0, 1 or 2"},
+    {"partition", &Options::partition, 0, 3, "partition must be 0, 1, 2 or 3"},
     {"hogwild_grid", &Options::hogwild_grid, 0, kMaxGrid, "hogwild_grid must be in [0, 64]"},
     {"balance", &Options::balance, 0, 2, "balance must be 0, 1 or 2"},
     {"sync_every", &Options::sync_every, 0, int64_t(1) << 30, "sync_every must be in [0, 2^30]"},
@@ -872,6 +872,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;
         a.sched = c.sched;
+        a.free_run = hog && g_opt.partition == 3 ? 1 : 0;
         a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
             CHK(grow(&c.trace, &c.trace_cap, (int64_t)s * s, "trace"));

@@ -55,6 +55,11 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 // (agent-scope release) before it advances the ticket, and a wavefront
 // entering a block invalidates its caches (agent-scope acquire) first.
 //
+// With free_run, blocks open without their ticket (batch-Hogwild!
+// partitioned over the XCDs without waiting): teams still walk their columns
+// in wavefront order, but a team that is ahead may share a column block with
+// one that lags, and that block's rows are then updated on two XCDs at once.
+//
 // Nothing waits for a particular workgroup: work is claimed, not assigned,
 // so workgroups that become resident late (or never, before the others
 // finish) are harmless, and the grid may be as large as the occupancy allows.
@@ -67,7 +72,7 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 template <int KP, typename T, int D, bool DBG, bool SKIP>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, const int32_t* __restrict__ tmap,
-                                                 const int32_t* __restrict__ xteams, int nx, int pool,
+                                                 const int32_t* __restrict__ xteams, int nx, int pool, int free_run,
                                                  uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
                                                  T* __restrict__ Q, float lr, float lp, float lq, int f,
                                                  uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
@@ -110,7 +115,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             cw = (int)__hip_atomic_load(cursor + lt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (cw < s) {
                 const int col = Cperm[(lt + Ooff[cw]) % s];
-                open = __hip_atomic_load(tickets + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= (uint32_t)cw;
+                open = free_run ||
+                       __hip_atomic_load(tickets + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= (uint32_t)cw;
             }
         }
         if (__builtin_amdgcn_ballot_w64(cw < s) == 0)
@@ -294,12 +300,12 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)a.sink);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)nullptr);
     }

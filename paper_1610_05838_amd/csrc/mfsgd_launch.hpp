@@ -39,6 +39,7 @@ struct EpochLaunch {
     const int32_t* tmap;   // per workgroup: home team << 16 | member, or -1 (idle)
     const int32_t* xteams; // per XCD x: [x * (kMaxGrid + 1)] = team count, then the teams placed on x
     int pool;              // 1: a wavefront also serves the other teams of its XCD
+    int free_run;          // 1: blocks open without waiting for their column ticket
     int wg_waves;    // wavefronts per workgroup
     void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
     uint64_t sigma_c, sigma_o;
