@@ -26,6 +26,7 @@ import csv
 import glob
 import json
 import os
+import shutil
 import statistics
 import subprocess
 import sys
@@ -63,9 +64,37 @@ def rows(path):
         return list(csv.DictReader(f))
 
 
+_DEMANGLED = {}
+
+
+def demangle(name: str) -> str:
+    """Itanium-mangled kernel names (rocprofv3 leaves some, e.g. _Float16
+    instantiations, undemangled) through c++filt; else the nested name."""
+    name = name.strip()
+    if not name.startswith("_Z"):
+        return name
+    if name not in _DEMANGLED:
+        out = ""
+        if shutil.which("c++filt"):
+            out = subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip()
+        if not out or out == name:
+            # _ZN<len><id><len><id>...: keep the identifiers before the template arguments
+            parts, i = [], 3 if name.startswith("_ZN") else 2
+            while i < len(name) and name[i].isdigit():
+                j = i
+                while name[j].isdigit():
+                    j += 1
+                n = int(name[i:j])
+                parts.append(name[j:j + n])
+                i = j + n
+            out = "::".join(parts) or name
+        _DEMANGLED[name] = out
+    return _DEMANGLED[name]
+
+
 def short(name: str) -> str:
     # "void mfsgd::k_hogwild<128, float, 4, false>(...)" -> "mfsgd::k_hogwild<128, float, 4, false>"
-    name = name.strip()
+    name = demangle(name)
     if name.startswith("void "):
         name = name[5:]
     depth, out = 0, []
