@@ -82,6 +82,7 @@ struct Context {
     Plan hw;                // internal plan of the XCD-partitioned batch-Hogwild!
     // planner scratch
     int64_t* counts = nullptr;
+    int64_t counts_cap = 0;
     int64_t* totals = nullptr;
     int64_t* bnd = nullptr; // 2 x (kMaxGrid + 1)
     unsigned long long* deg = nullptr;
@@ -505,10 +506,14 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
 {
     Context& c = g;
     pl.invalidate();
-    if (!c.counts) {
-        CHK(dalloc((void**)&c.counts, sizeof(int64_t) * kMaxGrid * kMaxGrid * kPlanChunks, "plan counts"));
+    // chunks: enough wavefronts to hide the scatter's latency on large sample arrays
+    int64_t chunks = (nnz + kPlanChunkSamples - 1) / kPlanChunkSamples;
+    chunks = std::min<int64_t>(std::max<int64_t>(chunks, kPlanChunksMin), kPlanChunksMax);
+    chunks = std::min<int64_t>(chunks, kPlanCountBytes / (int64_t)(sizeof(int64_t) * s * s));
+    chunks = std::max<int64_t>(256, chunks / 256 * 256);
+    CHK(grow(&c.counts, &c.counts_cap, (int64_t)s * s * chunks, "plan counts"));
+    if (!c.totals)
         CHK(dalloc((void**)&c.totals, sizeof(int64_t) * kMaxGrid * kMaxGrid, "plan totals"));
-    }
     if (!pl.bstart)
         CHK(dalloc((void**)&pl.bstart, sizeof(int64_t) * (kMaxGrid * kMaxGrid + 1), "plan starts"));
     CHK(grow(&pl.Sp, &pl.Sp_cap, nnz, "planned samples"));
@@ -563,7 +568,7 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     };
     pl.hot_row = hottest(du, cut.data());
     pl.hot_col = hottest(dv, ccut);
-    PlanBuffers b{c.counts, c.totals, pl.bstart, pl.Sp, keep_orig ? pl.orig : nullptr, c.bad, rbnd, cbnd};
+    PlanBuffers b{c.counts, (int)chunks, c.totals, pl.bstart, pl.Sp, keep_orig ? pl.orig : nullptr, c.bad, rbnd, cbnd};
     HIPCHK(plan_build(S, nnz, c.m, c.n, s, b, st));
     HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
     HIPCHK(hipStreamSynchronize(st));

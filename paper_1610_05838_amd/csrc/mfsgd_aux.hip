@@ -139,21 +139,70 @@ __device__ __forceinline__ int block_of(int u, int v, int64_t m, int64_t n, int 
     return rb * s + cb;
 }
 
-// Per-index sample counts (users and items) for the balanced cut; indices out
-// of range are skipped and flagged.
-__global__ void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
-                          unsigned long long* __restrict__ du, unsigned long long* __restrict__ dv, int* bad)
+// Per-index sample counts (users and items) for the balanced cut and the
+// hot-row/column measures; indices out of range are skipped and flagged.
+// A workgroup counts a tile of kDegTile samples into open-addressed LDS
+// tables (kDegSlots slots each, so at most half full: every probe sequence
+// ends), then adds each distinct index's count to global memory once.  Under
+// Zipf-like popularity one index can hold several percent of all samples;
+// per-sample global atomics on its counter would serialise.
+constexpr int kDegTile = 2048;
+constexpr int kDegSlots = 4096;
+static_assert(kDegSlots >= 2 * kDegTile, "degree tables must stay at most half full");
+
+__device__ __forceinline__ void deg_insert(int* keys, unsigned* cnt, int key)
 {
-    int found = 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * blockDim.x) {
-        const int u = __builtin_nontemporal_load(&S[i].u);
-        const int v = __builtin_nontemporal_load(&S[i].v);
-        if (u < 0 || u >= m || v < 0 || v >= n) {
-            found = 1;
-            continue;
+    unsigned h = ((unsigned)key * 2654435761u) >> 20; // 12 bits: kDegSlots = 4096
+    for (;;) {
+        const int old = atomicCAS(&keys[h], -1, key);
+        if (old == -1 || old == key) {
+            atomicAdd(&cnt[h], 1u);
+            return;
         }
-        atomicAdd(du + u, 1ull);
-        atomicAdd(dv + v, 1ull);
+        h = (h + 1) & (kDegSlots - 1);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_degrees(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
+                                                 unsigned long long* __restrict__ du,
+                                                 unsigned long long* __restrict__ dv, int* bad)
+{
+    __shared__ int ku[kDegSlots], kv[kDegSlots];
+    __shared__ unsigned cu[kDegSlots], cv[kDegSlots];
+    for (int j = threadIdx.x; j < kDegSlots; j += blockDim.x) {
+        ku[j] = kv[j] = -1;
+        cu[j] = cv[j] = 0u;
+    }
+    __syncthreads();
+    int found = 0;
+    const int64_t tiles = (nnz + kDegTile - 1) / kDegTile;
+    for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+        const int64_t lo = t * kDegTile;
+        const int64_t hi = lo + kDegTile < nnz ? lo + kDegTile : nnz;
+        for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+            const int u = __builtin_nontemporal_load(&S[i].u);
+            const int v = __builtin_nontemporal_load(&S[i].v);
+            if (u < 0 || u >= m || v < 0 || v >= n) {
+                found = 1;
+                continue;
+            }
+            deg_insert(ku, cu, u);
+            deg_insert(kv, cv, v);
+        }
+        __syncthreads();
+        for (int j = threadIdx.x; j < kDegSlots; j += blockDim.x) {
+            if (ku[j] >= 0) {
+                atomicAdd(du + ku[j], (unsigned long long)cu[j]);
+                ku[j] = -1;
+                cu[j] = 0u;
+            }
+            if (kv[j] >= 0) {
+                atomicAdd(dv + kv[j], (unsigned long long)cv[j]);
+                kv[j] = -1;
+                cv[j] = 0u;
+            }
+        }
+        __syncthreads();
     }
     if (found)
         atomicOr(bad, 1);
@@ -164,16 +213,16 @@ hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsi
 {
     if (nnz <= 0)
         return hipSuccess;
-    int64_t blocks = (nnz + 255) / 256;
-    if (blocks > 8192)
-        blocks = 8192;
+    int64_t blocks = (nnz + kDegTile - 1) / kDegTile;
+    if (blocks > 2048)
+        blocks = 2048;
     hipLaunchKernelGGL(k_degrees, dim3((unsigned)blocks), dim3(256), 0, st, S, nnz, m, n, du, dv, bad);
     return hipGetLastError();
 }
 
 __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
                                                    int s, const int64_t* rbnd, const int64_t* cbnd,
-                                                   int64_t* __restrict__ counts, int* bad)
+                                                   int64_t* __restrict__ counts, int chunks, int* bad)
 {
     __shared__ int hist[kMaxGrid * kMaxGrid];
     __shared__ Cut cut;
@@ -182,7 +231,7 @@ __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S,
         hist[i] = 0;
     load_cut(cut, rbnd, cbnd, s);
     __syncthreads();
-    const int64_t cs = (nnz + kPlanChunks - 1) / kPlanChunks;
+    const int64_t cs = (nnz + chunks - 1) / chunks;
     const int64_t lo = (int64_t)blockIdx.x * cs;
     const int64_t hi = lo + cs < nnz ? lo + cs : nnz;
     int found = 0;
@@ -199,22 +248,20 @@ __global__ __launch_bounds__(64) void k_plan_count(const Sample* __restrict__ S,
         atomicOr(bad, 1);
     __syncthreads();
     for (int b = threadIdx.x; b < nb; b += 64)
-        counts[(int64_t)b * kPlanChunks + blockIdx.x] = hist[b];
+        counts[(int64_t)b * chunks + blockIdx.x] = hist[b];
 }
 
-// exclusive scan of counts[b][0..kPlanChunks) in place, total to totals[b]
-__global__ __launch_bounds__(256) void k_plan_scan_chunks(int64_t* __restrict__ counts, int64_t* __restrict__ totals)
+// exclusive scan of counts[b][0..chunks) in place, total to totals[b]
+// (chunks is a multiple of 256; thread j scans chunks j*per .. j*per+per-1)
+__global__ __launch_bounds__(256) void k_plan_scan_chunks(int64_t* __restrict__ counts, int chunks,
+                                                          int64_t* __restrict__ totals)
 {
-    constexpr int per = kPlanChunks / 256;
+    const int per = chunks / 256;
     __shared__ int64_t part[256];
-    int64_t* row = counts + (int64_t)blockIdx.x * kPlanChunks;
-    int64_t local[per];
+    int64_t* row = counts + (int64_t)blockIdx.x * chunks + (int64_t)threadIdx.x * per;
     int64_t acc = 0;
-#pragma unroll
-    for (int i = 0; i < per; ++i) {
-        local[i] = row[threadIdx.x * per + i];
-        acc += local[i];
-    }
+    for (int i = 0; i < per; ++i)
+        acc += row[i];
     part[threadIdx.x] = acc;
     __syncthreads();
     // inclusive Hillis-Steele scan of the 256 thread sums
@@ -225,10 +272,10 @@ __global__ __launch_bounds__(256) void k_plan_scan_chunks(int64_t* __restrict__ 
         __syncthreads();
     }
     int64_t run = threadIdx.x > 0 ? part[threadIdx.x - 1] : 0;
-#pragma unroll
     for (int i = 0; i < per; ++i) {
-        row[threadIdx.x * per + i] = run;
-        run += local[i];
+        const int64_t x = row[i];
+        row[i] = run;
+        run += x;
     }
     if (threadIdx.x == 255)
         totals[blockIdx.x] = part[255];
@@ -270,7 +317,7 @@ __global__ __launch_bounds__(1024) void k_plan_scan_blocks(const int64_t* __rest
 
 __global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ S, int64_t nnz, int64_t m, int64_t n,
                                                      int s, const int64_t* rbnd, const int64_t* cbnd,
-                                                     const int64_t* __restrict__ counts,
+                                                     const int64_t* __restrict__ counts, int chunks,
                                                      const int64_t* __restrict__ bstart, Sample* __restrict__ Sp,
                                                      int64_t* __restrict__ orig)
 {
@@ -278,12 +325,12 @@ __global__ __launch_bounds__(64) void k_plan_scatter(const Sample* __restrict__ 
     __shared__ Cut cut;
     const int nb = s * s;
     for (int b = threadIdx.x; b < nb; b += 64)
-        base[b] = bstart[b] + counts[(int64_t)b * kPlanChunks + blockIdx.x];
+        base[b] = bstart[b] + counts[(int64_t)b * chunks + blockIdx.x];
     load_cut(cut, rbnd, cbnd, s);
     __syncthreads();
     const int lane = threadIdx.x;
     const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    const int64_t cs = (nnz + kPlanChunks - 1) / kPlanChunks;
+    const int64_t cs = (nnz + chunks - 1) / chunks;
     const int64_t lo = (int64_t)blockIdx.x * cs;
     const int64_t hi = lo + cs < nnz ? lo + cs : nnz;
     for (int64_t c0 = lo; c0 < hi; c0 += 64) {
@@ -326,9 +373,11 @@ hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s,
                       hipStream_t st)
 {
     const int nb = s * s;
-    hipLaunchKernelGGL(k_plan_count, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd, b.counts,
-                       b.bad);
-    hipLaunchKernelGGL(k_plan_scan_chunks, dim3(nb), dim3(256), 0, st, b.counts, b.totals);
+    if (b.chunks < 256 || b.chunks % 256 != 0)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_plan_count, dim3(b.chunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd, b.counts,
+                       b.chunks, b.bad);
+    hipLaunchKernelGGL(k_plan_scan_chunks, dim3(nb), dim3(256), 0, st, b.counts, b.chunks, b.totals);
     hipLaunchKernelGGL(k_plan_scan_blocks, dim3(1), dim3(1024), 0, st, b.totals, nb, b.bstart);
     return hipGetLastError();
 }
@@ -336,8 +385,8 @@ hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s,
 hipError_t plan_scatter(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
                         hipStream_t st)
 {
-    hipLaunchKernelGGL(k_plan_scatter, dim3(kPlanChunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd,
-                       b.counts, b.bstart, b.Sp, b.orig);
+    hipLaunchKernelGGL(k_plan_scatter, dim3(b.chunks), dim3(64), 0, st, S, nnz, m, n, s, b.rbnd, b.cbnd,
+                       b.counts, b.chunks, b.bstart, b.Sp, b.orig);
     return hipGetLastError();
 }
 

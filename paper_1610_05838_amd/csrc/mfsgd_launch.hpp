@@ -78,6 +78,7 @@ hipError_t probe_xcc(int* out, int n, hipStream_t st);
 // stable bucketing of samples into the s x s grid
 struct PlanBuffers {
     int64_t* counts;     // s*s*chunks, bin-major
+    int chunks;          // contiguous sample ranges counted and scattered in parallel (a multiple of 256)
     int64_t* totals;     // s*s
     int64_t* bstart;     // s*s+1
     Sample* Sp;          // planned copy
@@ -89,7 +90,12 @@ struct PlanBuffers {
 // per-index sample counts for the balanced cut (indices out of range raise *bad)
 hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsigned long long* du,
                         unsigned long long* dv, int* bad, hipStream_t st);
-constexpr int kPlanChunks = 2048;
+// chunks of a plan: about one per kPlanChunkSamples samples, between
+// kPlanChunksMin and kPlanChunksMax, and at most kPlanCountBytes of counts
+constexpr int kPlanChunksMin = 2048;
+constexpr int kPlanChunksMax = 16384;
+constexpr int64_t kPlanChunkSamples = 65536;
+constexpr int64_t kPlanCountBytes = int64_t(512) << 20;
 // counts, per-block scans and block starts; raises *b.bad on an index out of range
 hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
                       hipStream_t st);
