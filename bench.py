@@ -117,7 +117,7 @@ def main():
     ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det"])
     ap.add_argument("--grid-s", type=int, default=0, help="wavefront grid side (0: the workload's, else 32)")
     ap.add_argument("--workers", type=int, default=0)
-    ap.add_argument("--depth", type=int, default=4)
+    ap.add_argument("--depth", type=int, default=2)
     ap.add_argument("--team-waves", type=int, default=0)
     ap.add_argument("--partition", type=int, default=2, help="batch-Hogwild!: 0 one address space, 1 XCD-partitioned, 2 automatic")
     ap.add_argument("--ntrain", type=int, default=0, help="override the training size (0: the workload's)")

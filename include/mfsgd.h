@@ -107,9 +107,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *   "workers"      batch-Hogwild! wavefronts in total; 0 (default) = as many
  *                  as stay resident on the GPU.
  *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8
- *                  (default 4).  A wavefront forwards its own pending
+ *                  (default 2).  A wavefront forwards its own pending
  *                  updates, so depth never changes the serial semantics of
- *                  one worker.
+ *                  one worker; fewer samples in flight also means fresher
+ *                  reads of the rows other workers update.
  *   "team_waves"   wavefronts per wavefront-update worker; 0 (default) = as
  *                  many as stay resident, shared among the s workers in
  *                  proportion to the samples of their row blocks (each

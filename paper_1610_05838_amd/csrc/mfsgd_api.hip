@@ -22,7 +22,7 @@ struct Options {
     int64_t dtype = MFSGD_FP32;
     int64_t batch_f = 256;
     int64_t workers = 0;
-    int64_t depth = 4;
+    int64_t depth = 2;
     int64_t team_waves = 0;
     int64_t partition = 2;
     int64_t hogwild_grid = 0;

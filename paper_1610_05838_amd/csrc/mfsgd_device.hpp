@@ -87,10 +87,12 @@ struct Row {
 // Cross-lane sum over the 64 lanes; every lane receives the same value (each
 // step adds a pair of lanes in both orders, and IEEE addition commutes).
 // ---------------------------------------------------------------------------
+// (bound_ctrl set: the patterns below read only valid lanes, and it lets the
+// move fold into the add as one v_add_f32_dpp)
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float x)
 {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 
 __device__ __forceinline__ float wave_sum(float x)
@@ -335,11 +337,22 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         // a row that one of the previous D-1 samples rewrote is taken from that
         // sample's stored value (whole vectors; the nearest writer wins)
         V pv = st.sp[j], qv = st.sq[j];
+        // Wave-uniform test: where rows rarely repeat within D samples a
+        // scalar branch skips the selects; the hot-row variant (SKIP), whose
+        // rows repeat nearly every sample, always selects.
+        bool fwd = SKIP;
 #pragma unroll
-        for (int d = D - 1; d >= 1; --d) {
+        for (int d = 1; d < D && !SKIP; ++d) {
             const int h = (j - d + D) % D;
-            pv = pick(st.hu[h] == u, st.hp[h], pv);
-            qv = pick(st.hv[h] == v, st.hq[h], qv);
+            fwd |= (st.hu[h] == u) | (st.hv[h] == v);
+        }
+        if (__builtin_expect(fwd, 0)) {
+#pragma unroll
+            for (int d = D - 1; d >= 1; --d) {
+                const int h = (j - d + D) % D;
+                pv = pick(st.hu[h] == u, st.hp[h], pv);
+                qv = pick(st.hv[h] == v, st.hq[h], qv);
+            }
         }
         float p[E], q[E];
         R::widen(pv, p);
