@@ -120,7 +120,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
  *                  partitioned when P and Q together take at most 64 MiB
  *                  (they would otherwise sit in every XCD's L2 for the whole
- *                  epoch as diverging copies), one address space above that;
+ *                  epoch as diverging copies) or more than 256 MiB (beyond
+ *                  the Infinity Cache, where one address space sends every
+ *                  L2 miss to HBM), one address space in between;
  *                  3 partitioned without the column tickets: each worker
  *                  walks its column blocks in its wavefront order without
  *                  waiting, so workers that drift apart may share a column

@@ -170,7 +170,7 @@ def test_yahoo_shape_full_size(M, gen):
     T = gen.draw(w, w["ntrain"], w["ntest"])
     dT = M.samples_to_device(T)
     setup(M, w, debug=1)
-    assert M.get_option("partitioned") == 0  # 832 MB of factors: one address space
+    assert M.get_option("partitioned") == 1  # 832 MB of factors, beyond the Infinity Cache: partitioned
     hist = [M.rmse(dT)]
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
     assert bool(torch.all(M.debug_visits(w["ntrain"]) == 1))
