@@ -125,8 +125,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--workload", default="netflix")
     ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det"])
-    ap.add_argument("--kernel", default="", help="epoch kernel name (default: k_hogwild for one-address-space "
-                                                 "batch-Hogwild!, else k_blocked)")
+    ap.add_argument("--kernel", default="", help="epoch kernel name (default: whichever of k_hogwild and k_blocked "
+                                                 "takes more time in the trace)")
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--out", default="")
     ap.add_argument("--limit", type=int, default=400, help="seconds per rocprofv3 pass")
@@ -134,9 +134,7 @@ def main():
     ap.add_argument("bench_args", nargs=argparse.REMAINDER, help="after --: more bench.py options")
     a = ap.parse_args()
     extra = [x for x in a.bench_args if x != "--"]
-    kernel = a.kernel or ("k_hogwild" if a.scheme == "hogwild" and "--partition" not in extra else "k_blocked")
-    tag = f"{kernel}_{a.workload}" + ("" if a.scheme == "hogwild" else f"_{a.scheme}")
-    out = os.path.abspath(a.out or os.path.join(ROOT, "gpurun_out", f"prof_{tag}"))
+    out = os.path.abspath(a.out or os.path.join(ROOT, "gpurun_out", f"prof_{a.workload}_{a.scheme}"))
     py = sys.executable or "python3"
     base = [py, os.path.join(ROOT, "bench.py"), "--workload", a.workload, "--scheme", a.scheme,
             "--no-cpu-baseline"] + extra
@@ -162,6 +160,12 @@ def main():
 
     stats = rows(find_csv(os.path.join(out, "trace"), "kernel_stats.csv"))
     trace = rows(find_csv(os.path.join(out, "trace"), "kernel_trace.csv"))
+    kernel = a.kernel
+    if not kernel:
+        tot = {k: sum(float(r["TotalDurationNs"]) for r in stats if short(r["Name"]).split("<")[0].endswith(k))
+               for k in ("k_hogwild", "k_blocked")}
+        kernel = max(tot, key=tot.get)
+    tag = f"{kernel}_{a.workload}" + ("" if a.scheme == "hogwild" else f"_{a.scheme}")
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in trace
             if short(r["Kernel_Name"]).split("<")[0].endswith(kernel)]
     if not durs:
