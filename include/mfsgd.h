@@ -76,9 +76,10 @@ enum {
      * others as lines are written back and evicted (see "sync_every").  With
      * "partition" = 1 the rating matrix is cut into an s x s grid (s = number
      * of XCDs unless "hogwild_grid" says otherwise; planned internally, once
-     * per sample array) and one team of wavefronts per XCD runs
-     * batch-Hogwild! inside the block the wavefront schedule below gives it,
-     * so concurrent updates always meet in one L2. */
+     * per sample array) and the wavefronts of each XCD run batch-Hogwild!
+     * inside the block the wavefront schedule below gives that XCD's worker,
+     * each claiming the block's next batch when it is free, so concurrent
+     * updates always meet in one L2. */
     MFSGD_BATCH_HOGWILD = 0,
     /* wavefront-update (section 3.2.3) on the s x s grid of the last
      * mfsgd_plan: worker i owns row block i and visits the column blocks in
@@ -86,8 +87,12 @@ enum {
      * per epoch from (seed, epoch), so the blocks of one wave share no row and
      * no column.  A 1-D array of column tickets orders the waves: worker i
      * starts wave w once column sigma_i(w) has been released by wave w-1.  A
-     * worker is a team of "team_waves" wavefronts on one XCD running
-     * batch-Hogwild! inside the block. */
+     * worker lives on one XCD; inside its open block the wavefronts of that
+     * XCD claim batches of f samples one at a time and run them as
+     * batch-Hogwild!, and a wavefront with nothing to claim for its own
+     * worker serves the other workers of its XCD.  Work is claimed, not
+     * assigned, so the launch does not depend on every workgroup being
+     * resident at once. */
     MFSGD_WAVEFRONT = 1,
     /* the same schedule with one wavefront per worker and each block's
      * samples in their array order: the result then equals the serial
@@ -111,11 +116,13 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  updates, so depth never changes the serial semantics of
  *                  one worker; fewer samples in flight also means fresher
  *                  reads of the rows other workers update.
- *   "team_waves"   wavefronts per wavefront-update worker; 0 (default) = as
- *                  many as stay resident, shared among the s workers in
+ *   "team_waves"   wavefronts per wavefront-update worker (rounded up to
+ *                  whole workgroups of 4); 0 (default) = every workgroup slot
+ *                  the occupancy allows, shared among the s workers in
  *                  proportion to the samples of their row blocks (each
  *                  worker on one XCD, the XCDs loaded as evenly as the row
- *                  blocks allow).
+ *                  blocks allow).  A worker's wavefronts prefer its blocks
+ *                  but also serve the other workers on their XCD.
  *   "partition"    batch-Hogwild!: 0 one address space, 1 partitioned over
  *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
  *                  partitioned when P and Q together take at most 64 MiB
