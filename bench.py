@@ -126,6 +126,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--staged", action="store_true",
+                    help="training samples stay in pinned host memory and stream through the GPU (mfsgd_epoch_staged, "
+                         "batch-Hogwild!): value then includes the PCIe transfers and is not the resident rate")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -147,7 +150,13 @@ def main():
     if args.ntrain:
         w["ntrain"] = args.ntrain
     t0 = time.perf_counter()
-    if w["draw"] == "independent":
+    if args.staged:
+        if args.scheme != "hogwild":
+            raise SystemExit("--staged runs batch-Hogwild! only")
+        S = datagen.draw(w, 0, w["ntrain"]) if w["draw"] == "independent" else datagen.make(w)[0]
+        T = datagen.draw(w, w["ntrain"], w["ntest"]) if w["draw"] == "independent" else datagen.make(w)[1]
+        dS = torch.from_numpy(S.view(np.int32).reshape(-1, 3)).pin_memory()
+    elif w["draw"] == "independent":
         # generated chunk by chunk straight into HBM; the host keeps a prefix for the CPU baseline
         dS = datagen.draw_to_device(w, 0, w["ntrain"], dev, progress=lambda a, b: (
             log(f"  generated {a}/{b}") if a % (1 << 29) < (1 << 25) else None))
@@ -170,7 +179,7 @@ def main():
         mfsgd.set_option(key, int(val))
     mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
     resident = mfsgd.get_option("resident_waves")
-    partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1
+    partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged
     kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
     grid_s = args.grid_s or w.get("grid_s", 32)
     if args.scheme != "hogwild":
@@ -183,7 +192,10 @@ def main():
         lr = datagen.lr_at(w, t)
         if ev is not None:
             ev[0].record(stream)
-        mfsgd.epoch(dS, lr, w["lam"], w["lam"], args.scheme, stream)
+        if args.staged:
+            mfsgd.epoch_staged(dS, lr, w["lam"], w["lam"], stream)
+        else:
+            mfsgd.epoch(dS, lr, w["lam"], w["lam"], args.scheme, stream)
         if ev is not None:
             ev[1].record(stream)
         return mfsgd.rmse(dT, stream)
@@ -238,6 +250,7 @@ def main():
                                f"{w['dtype']} {args.scheme}" + (f" s={grid_s}" if args.scheme != "hogwild"
                                                                  else " f=256"),
                    "scheme": args.scheme, "partitioned": partitioned, "workers": args.workers or "auto",
+                   "staged": args.staged,
                    "resident_waves": resident,
                    "depth": args.depth, "epochs_timed": args.steps},
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",

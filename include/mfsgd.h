@@ -163,6 +163,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  half of the samples of its row or column block (many
  *                  wavefronts then update one row at once).  Epochs with
  *                  debug output never skip.
+ *   "stage_samples" samples per chunk of mfsgd_epoch_staged (default 2^25,
+ *                  402 MB per buffer; three device buffers, and three
+ *                  pinned host buffers for pageable arrays).
  *   "debug"        bit 0: count visits of every sample (read with
  *                  mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
  *                  schedule (MFSGD_DBG_TRACE).  Costs one extra atomic per
@@ -212,6 +215,29 @@ int mfsgd_plan(const mfsgd_sample* samples, int64_t nnz, int32_t s, void* stream
  * wavefront scheme without a plan for these samples. */
 int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
                 int32_t scheme, void* stream);
+
+/* One batch-Hogwild! epoch over samples that stay in host memory, for sample
+ * arrays larger than the GPU's memory: the out-of-core mode of section 4,
+ * where the transfer of the next part of R overlaps the computation on the
+ * current one.  The array is cut into chunks of "stage_samples" consecutive
+ * samples (rounded down to a multiple of f); chunk i is copied into one of
+ * three library-owned device buffers on a library-owned stream while the
+ * kernel of chunk i-1 runs on `stream`, and each chunk is run like
+ * MFSGD_BATCH_HOGWILD in one address space (batch b of the chunk to worker
+ * b mod W, chunks in array order).  With one worker this is exactly the
+ * serial update in array order.
+ * samples: host memory, caller-owned, 12-byte records as for mfsgd_epoch.
+ * Pinned memory (hipHostMalloc) is copied directly and must stay valid and
+ * unchanged until the work on `stream` completes; pageable memory is copied
+ * by this thread into pinned staging buffers, so the call returns once its
+ * last chunk has been staged.  Asynchronous on `stream` otherwise;
+ * increments the epoch counter.  Indices are not checked (use
+ * mfsgd_check_samples on a device copy).  Debug bit 0 counts visits as for
+ * mfsgd_epoch.
+ * EINVAL: nnz < 0, NULL samples with nnz > 0, a device pointer, non-finite
+ * lr or lambda.  ESTATE: no init.  ENOMEM: staging buffers. */
+int mfsgd_epoch_staged(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
+                       void* stream);
 
 /* Test RMSE (section 3.2.4): sqrt(sum over the ntest samples of
  * (r - p_u . q_v)^2 / ntest), dot products in binary32, squares summed in

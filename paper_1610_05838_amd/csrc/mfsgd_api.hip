@@ -31,6 +31,7 @@ struct Options {
     int64_t sync_l1 = 0;
     int64_t spin_limit = int64_t(1) << 24;
     int64_t skip_stores = 2;
+    int64_t stage_samples = int64_t(1) << 25;
     int64_t debug = 0;
 };
 
@@ -99,6 +100,14 @@ struct Context {
     int32_t* xteams = nullptr; // kMaxGrid * (kMaxGrid + 1): per XCD, team count then teams
     unsigned char* sink = nullptr; // rows for skipped stores, 2 per wavefront of the grid
     int64_t sink_cap = 0;
+    // staged epochs: a ring of device buffers fed from host memory by a copy stream
+    static constexpr int kStages = 3;
+    Sample* stage_dev[kStages] = {};
+    Sample* stage_host[kStages] = {}; // pinned, only for pageable caller arrays
+    int64_t stage_dev_cap = 0, stage_host_cap = 0;
+    hipStream_t copy_stream = nullptr;
+    hipEvent_t ev_copied[kStages] = {}, ev_used[kStages] = {}, ev_start = nullptr;
+    bool copied_pending[kStages] = {};
     const Plan* lay_plan = nullptr;
     uint64_t lay_version = 0;
     int64_t lay_want = -1;
@@ -211,6 +220,19 @@ void release_all()
     dfree(c.tsize);
     dfree(c.xteams);
     dfree(c.sink);
+    for (int i = 0; i < Context::kStages; ++i) {
+        dfree(c.stage_dev[i]);
+        if (c.stage_host[i])
+            (void)hipHostFree(c.stage_host[i]);
+        if (c.ev_copied[i])
+            (void)hipEventDestroy(c.ev_copied[i]);
+        if (c.ev_used[i])
+            (void)hipEventDestroy(c.ev_used[i]);
+    }
+    if (c.ev_start)
+        (void)hipEventDestroy(c.ev_start);
+    if (c.copy_stream)
+        (void)hipStreamDestroy(c.copy_stream);
     c = Context();
 }
 
@@ -305,6 +327,7 @@ const OptSpec kOpts[] = {
     {"sync_l1", &Options::sync_l1, 0, 1, "sync_l1 must be 0 or 1"},
     {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
     {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
+    {"stage_samples", &Options::stage_samples, 64, int64_t(1) << 31, "stage_samples must be in [64, 2^31]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
 };
 
@@ -900,6 +923,145 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
     return MFSGD_OK;
 }
 
+// ---------------------------------------------------------------------------
+// staged epochs (samples in host memory)
+// ---------------------------------------------------------------------------
+// The sample array is cut into chunks of C consecutive samples (C = option
+// "stage_samples" rounded down to a multiple of f).  Chunk i is copied into
+// device buffer i mod 3 on the library's copy stream while the caller's
+// stream runs the batch-Hogwild! kernel (one address space) over chunk i-1;
+// events order each copy after the kernel that last read its buffer and
+// each kernel after its copy.  A pinned caller array is copied directly; a
+// pageable one passes through pinned staging buffers, filled by this thread
+// once the copy that last read them has finished.
+int staged_buffers(int64_t C, bool pageable)
+{
+    Context& c = g;
+    if (!c.copy_stream) {
+        HIPCHK(hipStreamCreateWithFlags(&c.copy_stream, hipStreamNonBlocking));
+        HIPCHK(hipEventCreateWithFlags(&c.ev_start, hipEventDisableTiming));
+        for (int i = 0; i < Context::kStages; ++i) {
+            HIPCHK(hipEventCreateWithFlags(&c.ev_copied[i], hipEventDisableTiming));
+            HIPCHK(hipEventCreateWithFlags(&c.ev_used[i], hipEventDisableTiming));
+        }
+    }
+    if (c.stage_dev_cap < C) {
+        HIPCHK(hipDeviceSynchronize()); // no kernel may still read the old buffers
+        for (int i = 0; i < Context::kStages; ++i) {
+            dfree(c.stage_dev[i]);
+            c.stage_dev[i] = nullptr;
+        }
+        c.stage_dev_cap = 0;
+        for (int i = 0; i < Context::kStages; ++i)
+            CHK(dalloc((void**)&c.stage_dev[i], sizeof(Sample) * (size_t)C, "staging buffers"));
+        c.stage_dev_cap = C;
+    }
+    if (pageable && c.stage_host_cap < C) {
+        for (int i = 0; i < Context::kStages; ++i) {
+            if (c.copied_pending[i])
+                HIPCHK(hipEventSynchronize(c.ev_copied[i]));
+            c.copied_pending[i] = false;
+            if (c.stage_host[i])
+                (void)hipHostFree(c.stage_host[i]);
+            c.stage_host[i] = nullptr;
+        }
+        c.stage_host_cap = 0;
+        for (int i = 0; i < Context::kStages; ++i)
+            if (hipHostMalloc((void**)&c.stage_host[i], sizeof(Sample) * (size_t)C, hipHostMallocDefault) !=
+                hipSuccess) {
+                (void)hipGetLastError();
+                return fail(MFSGD_ENOMEM, "pinned staging allocation failed");
+            }
+        c.stage_host_cap = C;
+    }
+    return MFSGD_OK;
+}
+
+int epoch_staged_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, float lq, hipStream_t st)
+{
+    Context& c = g;
+    if (!c.inited)
+        return fail(MFSGD_ESTATE, "mfsgd_init has not been called");
+    if (!valid_samples(samples, nnz))
+        return fail(MFSGD_EINVAL, "bad sample array");
+    if (!std::isfinite(lr) || !std::isfinite(lp) || !std::isfinite(lq))
+        return fail(MFSGD_EINVAL, "lr and lambdas must be finite");
+    bool pinned = false;
+    if (nnz > 0) {
+        hipPointerAttribute_t attr{};
+        if (hipPointerGetAttributes(&attr, samples) == hipSuccess) {
+            if (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeArray)
+                return fail(MFSGD_EINVAL, "mfsgd_epoch_staged takes host memory; use mfsgd_epoch for device samples");
+            pinned = attr.type == hipMemoryTypeHost;
+        } else {
+            (void)hipGetLastError(); // plain pageable memory is unknown to the runtime
+        }
+    }
+    const int64_t f = g_opt.batch_f;
+    const int64_t C = std::max<int64_t>(f, g_opt.stage_samples / f * f);
+    const int64_t dbg = g_opt.debug;
+    EpochLaunch a{};
+    a.scheme = kSchemeHogwild;
+    a.KP = c.KP;
+    a.depth = (int)g_opt.depth;
+    a.f = (int)f;
+    a.P = c.P;
+    a.Q = c.Q;
+    a.lr = lr;
+    a.lp = lp;
+    a.lq = lq;
+    a.nx = c.nx;
+    int64_t W = g_opt.workers;
+    if (W == 0) {
+        const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);
+        if (per_cu <= 0)
+            return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
+        W = (int64_t)c.cus * per_cu;
+    }
+    if (dbg & 1) {
+        CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
+        c.visits_n = nnz;
+        HIPCHK(hipMemsetAsync(c.visits, 0, sizeof(uint32_t) * (size_t)(nnz > 0 ? nnz : 1), st));
+    }
+    if (nnz > 0) {
+        CHK(staged_buffers(std::min(C, nnz), !pinned));
+        // copies start after everything already queued on the caller's stream
+        // (a previous epoch's kernels may still read the device buffers)
+        HIPCHK(hipEventRecord(c.ev_start, st));
+        HIPCHK(hipStreamWaitEvent(c.copy_stream, c.ev_start, 0));
+        const char* src = (const char*)samples;
+        for (int64_t i = 0, off = 0; off < nnz; ++i, off += C) {
+            const int64_t cnt = std::min(C, nnz - off);
+            const int b = (int)(i % Context::kStages);
+            if (i >= Context::kStages)
+                HIPCHK(hipStreamWaitEvent(c.copy_stream, c.ev_used[b], 0));
+            const void* from = src + (size_t)off * sizeof(Sample);
+            if (!pinned) {
+                if (c.copied_pending[b])
+                    HIPCHK(hipEventSynchronize(c.ev_copied[b]));
+                std::memcpy(c.stage_host[b], from, sizeof(Sample) * (size_t)cnt);
+                from = c.stage_host[b];
+            }
+            HIPCHK(hipMemcpyAsync(c.stage_dev[b], from, sizeof(Sample) * (size_t)cnt, hipMemcpyHostToDevice,
+                                  c.copy_stream));
+            HIPCHK(hipEventRecord(c.ev_copied[b], c.copy_stream));
+            c.copied_pending[b] = !pinned;
+            HIPCHK(hipStreamWaitEvent(st, c.ev_copied[b], 0));
+            a.S = c.stage_dev[b];
+            a.nnz = cnt;
+            a.W = std::min(W, (cnt + f - 1) / f);
+            a.visits = (dbg & 1) ? c.visits + off : nullptr;
+            if (c.dtype == MFSGD_FP16)
+                HIPCHK(epoch_f16(a, st));
+            else
+                HIPCHK(epoch_f32(a, st));
+            HIPCHK(hipEventRecord(c.ev_used[b], st));
+        }
+    }
+    c.epoch += 1;
+    return MFSGD_OK;
+}
+
 int rmse_impl(const mfsgd_sample* test, int64_t ntest, double* out, hipStream_t st)
 {
     Context& c = g;
@@ -1014,6 +1176,13 @@ int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda
 {
     return guarded(
         [&]() -> int { return epoch_impl(samples, nnz, lr, lambda_p, lambda_q, scheme, (hipStream_t)stream); });
+}
+
+int mfsgd_epoch_staged(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
+                       void* stream)
+{
+    return guarded(
+        [&]() -> int { return epoch_staged_impl(samples, nnz, lr, lambda_p, lambda_q, (hipStream_t)stream); });
 }
 
 int mfsgd_rmse(const mfsgd_sample* test, int64_t ntest, double* rmse_out, void* stream)

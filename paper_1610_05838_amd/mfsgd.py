@@ -55,6 +55,7 @@ def lib():
             "mfsgd_init": ([i64, i64, i32, u64], C.c_int),
             "mfsgd_plan": ([vp, i64, i32, vp], C.c_int),
             "mfsgd_epoch": ([vp, i64, f32, f32, f32, i32, vp], C.c_int),
+            "mfsgd_epoch_staged": ([vp, i64, f32, f32, f32, vp], C.c_int),
             "mfsgd_rmse": ([vp, i64, C.POINTER(C.c_double), vp], C.c_int),
             "mfsgd_check_samples": ([vp, i64, vp], C.c_int),
             "mfsgd_sync": ([vp], C.c_int),
@@ -129,6 +130,22 @@ def epoch(samples: torch.Tensor, lr: float, lambda_p: float, lambda_q: float, sc
     p, nnz = _samples_ptr(samples)
     sc = SCHEMES[scheme] if isinstance(scheme, str) else int(scheme)
     _check(lib().mfsgd_epoch(p, nnz, lr, lambda_p, lambda_q, sc, _stream(stream)), "mfsgd_epoch")
+
+
+def epoch_staged(samples, lr: float, lambda_p: float, lambda_q: float, stream=None) -> None:
+    """mfsgd_epoch_staged on host samples: a numpy (u, v, r) record array or
+    an int32 (nnz, 3) CPU tensor (pinned or not).  A pinned array must stay
+    alive and unchanged until the work on `stream` completes."""
+    if isinstance(samples, np.ndarray):
+        if samples.dtype != SAMPLE_DTYPE or not samples.flags["C_CONTIGUOUS"]:
+            raise TypeError("samples must be a C-contiguous array of (u, v, r) records")
+        p, nnz = C.c_void_p(samples.ctypes.data if samples.size else 0), samples.shape[0]
+    else:
+        t = samples
+        if t.dtype != torch.int32 or t.dim() != 2 or t.shape[1] != 3 or not t.is_contiguous() or t.is_cuda:
+            raise TypeError("samples must be a contiguous int32 CPU tensor of shape (nnz, 3)")
+        p, nnz = C.c_void_p(t.data_ptr() if t.numel() else 0), t.shape[0]
+    _check(lib().mfsgd_epoch_staged(p, nnz, lr, lambda_p, lambda_q, _stream(stream)), "mfsgd_epoch_staged")
 
 
 def rmse(test: torch.Tensor, stream=None) -> float:
