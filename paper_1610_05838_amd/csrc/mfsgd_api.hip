@@ -283,6 +283,13 @@ int sync_and_check(hipStream_t st)
 
 bool valid_samples(const mfsgd_sample* s, int64_t nnz) { return nnz >= 0 && (nnz == 0 || s != nullptr); }
 
+// whether every row of P and Q starts below 2^31 bytes (buffer addressing)
+bool rows_fit_31_bits()
+{
+    const int64_t row = (int64_t)g.KP * (int64_t)elem_size(g.dtype);
+    return std::max(g.m, g.n) * row <= (int64_t(1) << 31);
+}
+
 // Whether batch-Hogwild! runs partitioned over the XCDs.  Automatic choice:
 // Automatic choice of the batch-Hogwild! form by the size of P and Q:
 // up to kPartitionBytes they stay resident in every XCD's L2 for the whole
@@ -853,6 +860,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
     a.lq = lq;
     a.spin_limit = (uint32_t)g_opt.spin_limit;
     a.err = c.err;
+    a.buf = rows_fit_31_bits() ? 1 : 0;
     if (dbg & 1) {
         CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
         c.visits_n = nnz;
@@ -1011,6 +1019,7 @@ int epoch_staged_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float 
     a.lp = lp;
     a.lq = lq;
     a.nx = c.nx;
+    a.buf = rows_fit_31_bits() ? 1 : 0;
     int64_t W = g_opt.workers;
     if (W == 0) {
         const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);

@@ -83,6 +83,33 @@ struct Row {
     __device__ __forceinline__ static void store(T* p, const float (&x)[E]) { st(p, narrow(x)); }
 };
 
+// Buffer addressing for rows whose per-lane part is one dword (binary16 at
+// KP = 128, binary32 at KP <= 64): a descriptor for the whole matrix, the
+// lane's byte offset in a VGPR (loop-invariant) and the row's byte offset in
+// an SGPR, so a row access needs no vector address arithmetic.  Used only
+// when every row offset fits 31 bits.  (The descriptor's fourth word selects
+// 32-bit data, which raw loads and stores require; the record count is the
+// largest, so the hardware range check never clips.)
+struct Buf {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ explicit Buf(const void* base)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7FFFFFFF, 0x00020000))
+    {
+    }
+    template <typename V>
+    __device__ __forceinline__ V ld(uint32_t voff, uint32_t soff) const
+    {
+        static_assert(sizeof(V) == 4, "one dword per lane");
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+    }
+    template <typename V>
+    __device__ __forceinline__ void st(V v, uint32_t voff, uint32_t soff) const
+    {
+        static_assert(sizeof(V) == 4, "one dword per lane");
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, (int)voff, (int)soff, 0);
+    }
+};
+
 // ---------------------------------------------------------------------------
 // Cross-lane sum over the 64 lanes; every lane receives the same value (each
 // step adds a pair of lanes in both orders, and IEEE addition commutes).
@@ -265,13 +292,14 @@ struct WorkerState {
     int hu[D], hv[D];
 };
 
-template <int KP, typename T, int D, bool DBG, bool SKIP = false>
+template <int KP, typename T, int D, bool DBG, bool SKIP = false, bool BUF = false>
 __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t worker,
                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
                                            float lq, const DebugSink dbg, const CacheSync sync = CacheSync{0, false, false},
                                            T* sink = nullptr)
 {
     constexpr int E = Geo<KP>::E;
+    static_assert(!BUF || (!SKIP && sizeof(T) * E == 4), "buffer rows: one dword per lane, no store redirection");
     constexpr int A = Geo<KP>::A;
     typedef Row<T, E> R;
     static_assert(64 % D == 0 && D <= 32, "depth must divide 64");
@@ -279,6 +307,9 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
     const int lane = lane_id();
     // lanes past the row width (KP = 32) mirror lane 0's address and never store
     const int col = (A == 64 || lane < A) ? lane * E : 0;
+    const Buf bp(P), bq(Q);
+    const uint32_t cb = (uint32_t)(col * sizeof(T));        // lane's byte offset in a row
+    constexpr uint32_t kRowBytes = (uint32_t)(KP * sizeof(T));
     const bool holds = (A == 64) || (lane < A);
 
     int64_t c_batch = worker, n_batch = worker;
@@ -327,8 +358,13 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         st.su[slot] = ok ? u : -1;
         st.sv[slot] = ok ? v : -1;
         st.sr[slot] = r;
-        st.sp[slot] = R::ld(P + (int64_t)(ok ? u : 0) * KP + col);
-        st.sq[slot] = R::ld(Q + (int64_t)(ok ? v : 0) * KP + col);
+        if constexpr (BUF) {
+            st.sp[slot] = bp.template ld<V>(cb, (uint32_t)(ok ? u : 0) * kRowBytes);
+            st.sq[slot] = bq.template ld<V>(cb, (uint32_t)(ok ? v : 0) * kRowBytes);
+        } else {
+            st.sp[slot] = R::ld(P + (int64_t)(ok ? u : 0) * KP + col);
+            st.sq[slot] = R::ld(Q + (int64_t)(ok ? v : 0) * KP + col);
+        }
     };
 
     // update the sample in slot j
@@ -394,8 +430,13 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
             qbase = q_again ? sink + KP : qbase;
         }
         if (holds) {
-            R::st(pbase + col, np);
-            R::st(qbase + col, nq);
+            if constexpr (BUF) {
+                bp.template st<V>(np, cb, (uint32_t)u * kRowBytes);
+                bq.template st<V>(nq, cb, (uint32_t)v * kRowBytes);
+            } else {
+                R::st(pbase + col, np);
+                R::st(qbase + col, nq);
+            }
         }
         st.hu[j] = u;
         st.hv[j] = v;

@@ -13,7 +13,7 @@ constexpr int kHogwildBlock = 256; // 4 wavefronts per workgroup, each an indepe
 // wavefront w of the grid is worker w.  The XCDs' L2 caches are not coherent
 // with each other, so rows that several XCDs touch are updated in per-XCD
 // copies until evicted; the block-scheduled kernel below is the coherent form.
-template <int KP, typename T, int D, bool DBG>
+template <int KP, typename T, int D, bool DBG, bool BUF = false>
 __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restrict__ S, int64_t nnz, int64_t W,
                                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr,
                                                            float lp, float lq, DebugSink dbg, int sync_every,
@@ -25,7 +25,7 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
     // workgroups are dealt to XCDs round-robin: the first wavefront of each of
     // the first nx workgroups leads its XCD's cache flushes
     const CacheSync sync{sync_every, (int)blockIdx.x < nx && (threadIdx.x >> 6) == 0, sync_l1 != 0};
-    run_worker<KP, T, D, DBG>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
+    run_worker<KP, T, D, DBG, false, BUF>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
 }
 
 // Block-scheduled epoch: wavefront-update (section 3.2.3), and
@@ -293,6 +293,15 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
     if (a.scheme == kSchemeHogwild) {
         const int64_t blocks = (a.W + 3) / 4;
         const DebugSink dbg{a.visits, nullptr, a.trace_batch};
+        constexpr bool kDword = sizeof(T) * Geo<KP>::E == 4; // one dword of a row per lane
+        if constexpr (kDword && !DBG) {
+            if (a.buf) {
+                hipLaunchKernelGGL((k_hogwild<KP, T, D, false, true>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0,
+                                   st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1,
+                                   a.nx);
+                return hipGetLastError();
+            }
+        }
         hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st, a.S,
                            a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
     } else {

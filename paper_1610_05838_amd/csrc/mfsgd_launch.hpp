@@ -32,6 +32,7 @@ struct EpochLaunch {
     int sync_every;  // one-address-space batch-Hogwild!: batches between XCD cache flushes (0 = none)
     int sync_l1;     // ... and whether the other wavefronts drop their CU's L1 then
     int nx;          // XCDs (one-address-space batch-Hogwild!: the first nx workgroups lead the flushes)
+    int buf;         // every row offset of P and Q fits 31 bits: rows may be addressed through buffer descriptors
     // block-scheduled epochs
     const int64_t* bstart;
     int s;           // grid side
