@@ -375,10 +375,15 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         V pv = st.sp[j], qv = st.sq[j];
         // Wave-uniform test: where rows rarely repeat within D samples a
         // scalar branch skips the selects; the hot-row variant (SKIP), whose
-        // rows repeat nearly every sample, always selects.
-        bool fwd = SKIP;
+        // rows repeat nearly every sample, always selects.  So do lanes
+        // holding more than 16 bytes of a row (binary32 at KP = 512): the
+        // branched form of those produced wrong values at depths 2 and 4 in
+        // this compiler (caught by the single-worker parity tests), the
+        // always-select form is exact.
+        constexpr bool kAlways = SKIP || sizeof(V) > 16;
+        bool fwd = kAlways;
 #pragma unroll
-        for (int d = 1; d < D && !SKIP; ++d) {
+        for (int d = 1; d < D && !kAlways; ++d) {
             const int h = (j - d + D) % D;
             fwd |= (st.hu[h] == u) | (st.hv[h] == v);
         }

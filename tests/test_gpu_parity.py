@@ -124,7 +124,7 @@ def forwarding_stress(rng, nnz):
 
 @pytest.mark.parametrize("depth", [1, 2, 4, 8])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-@pytest.mark.parametrize("k", [32, 100, 128, 256])
+@pytest.mark.parametrize("k", [32, 50, 100, 128, 256, 300])  # padded widths 32, 64, 128, 128, 256, 512
 def test_single_worker_equals_serial(M, depth, dtype, k):
     rng = np.random.default_rng(depth * 1000 + k)
     for m, n, nnz in ((7, 5, 2000), (400, 300, 6001)):
@@ -337,6 +337,26 @@ def test_wavefront_det_k128_zipf(M, gen, skip):
     oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0, balanced=True)
     P, Q = factors(M, m, n, k, np.float32)
     assert maxabs(P, Po) <= 1e-4 and maxabs(Q, Qo) <= 1e-4
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [50, 300])
+def test_wavefront_det_other_widths(M, dtype, k):
+    """The block-scheduled kernel at padded widths 64 and 512 (one and eight
+    values per lane), deterministic schedule on an 8 x 8 grid, skipped stores
+    forced on: equal to the oracle's wave order."""
+    rng = np.random.default_rng(k)
+    m, n, seed, s = 900, 700, 5 + k, 8
+    S = rand_samples(rng, m, n, 60_000)
+    S["v"][::3] = 7  # one hot item: runs of one row inside its column's blocks
+    setup(M, m, n, k, seed, dtype, skip_stores=1)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    M.epoch(dS, 0.01, 0.05, 0.04, "wavefront_det")
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    oracle.epoch_wavefront(Po, Qo, S, 0.01, 0.05, 0.04, s, seed, 0, balanced=True)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
 
 def test_checkpoint_resume_is_bitwise(M, gen):
