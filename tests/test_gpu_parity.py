@@ -359,6 +359,26 @@ def test_wavefront_det_other_widths(M, dtype, k):
     assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("skip", [0, 1])
+@pytest.mark.parametrize("depth", [1, 4, 8])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_wavefront_det_depths(M, gen, dtype, depth, skip):
+    """The block-scheduled kernel at every prefetch depth (the default is 2),
+    with and without skipped stores: equal to the oracle's wave order on the
+    tiny workload with an 8 x 8 grid."""
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    m, n, k, seed, s = w["m"], w["n"], w["k"], w["seed"], 8
+    setup(M, m, n, k, seed, dtype, depth=depth, skip_stores=skip, balance=1)
+    dS = M.samples_to_device(S)
+    M.plan(dS, s)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0, balanced=True)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+
+
 def test_checkpoint_resume_is_bitwise(M, gen):
     import torch
     w = gen.workload("tiny")
