@@ -219,10 +219,15 @@ def main():
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
-        for _ in range(3):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        for i in range(3):
             b.copy_(a)
+            ev[i + 1].record(stream)
         torch.cuda.synchronize()
-        log("copy calibration: 3 x 4 GiB device copies done")
+        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
+        log("copy calibration: 3 x 4 GiB device copies, " + ", ".join(
+            f"{x:.2f} ms ({2 * a.numel() * 4 / x / 1e6:.0f} GB/s read+write)" for x in ms))
 
     bytes_per_update = 4 * w["k"] * feat_bytes + 12
     avg_epoch_s = sum(epoch_ms) / len(epoch_ms) / 1e3

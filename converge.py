@@ -1,0 +1,229 @@
+"""Convergence and scalability experiments on one MI355X (the analogues of the
+paper's schedule comparison, section 3.2.4, and of its updates/s-versus-
+workers figures).
+
+  python converge.py curves  [--workload netflix_fp16] [--epochs 20] [--lr config|paper]
+                             [--schemes hogwild,wavefront:8,wavefront:32] [--target 0.92]
+      Test RMSE after every epoch and the cumulative epoch-kernel time, per
+      schedule, from the same initial factors; prints the epoch and the time at
+      which each schedule first reaches --target.
+
+  python converge.py workers [--workload netflix_fp16] [--counts 64,128,...,8192]
+                             [--schemes hogwild,wavefront:32]
+      Updates/s of the epoch kernel against the number of concurrent workers
+      (wavefronts), one warm-up and --epochs timed epochs per point; a count
+      of 0 is the library's default launch.
+
+Learning rates: "config" is the workload's own schedule (lr * decay^t);
+"paper" is the decaying schedule of the evaluation section,
+s_t = alpha / (1 + beta * t^1.5), with the per-dataset alpha, beta and lambda
+of its parameter table (the Netflix row for the Netflix-shaped sets).
+
+Every run prints one JSON line per measurement, then a markdown table.  The
+data are the seeded synthetic sets of paper_1610_05838_amd.datagen.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# Parameter table of the evaluation section: (lambda, alpha, beta) per dataset.
+PAPER_PARAMS = {"netflix": (0.05, 0.08, 0.3), "yahoo": (1.0, 0.08, 0.2), "hugewiki": (0.03, 0.08, 0.3)}
+
+
+def log(msg):
+    print(f"[converge] {msg}", file=sys.stderr, flush=True)
+
+
+def stand_in(name: str) -> str:
+    """The dataset a synthetic workload stands in for."""
+    for d in PAPER_PARAMS:
+        if name.startswith(d):
+            return d
+    raise SystemExit(f"no parameter row for workload {name!r}")
+
+
+def lr_schedule(w: dict, kind: str):
+    """(lr(t), lambda) for the chosen schedule."""
+    from paper_1610_05838_amd import datagen
+
+    if kind == "config":
+        return (lambda t: datagen.lr_at(w, t)), w["lam"]
+    lam, alpha, beta = PAPER_PARAMS[stand_in(w["name"])]
+    return (lambda t: alpha / (1.0 + beta * t ** 1.5)), lam
+
+
+def parse_schemes(text: str):
+    out = []
+    for item in text.split(","):
+        name, _, s = item.partition(":")
+        if name not in ("hogwild", "wavefront", "wavefront_det"):
+            raise SystemExit(f"unknown scheme {name!r}")
+        out.append((name, int(s) if s else 0))
+    return out
+
+
+def label(scheme, s):
+    return scheme if scheme == "hogwild" else f"{scheme} s={s}"
+
+
+class Runner:
+    """Holds the device copies of one workload's train and test sets."""
+
+    def __init__(self, workload: str):
+        import torch
+
+        from paper_1610_05838_amd import datagen, mfsgd
+
+        assert torch.cuda.is_available(), "converge.py needs a GPU"
+        self.torch, self.datagen, self.M = torch, datagen, mfsgd
+        self.dev = torch.device("cuda:0")
+        torch.cuda.set_device(self.dev)
+        w = datagen.workload(workload)
+        t0 = time.perf_counter()
+        if w["draw"] == "independent":
+            self.dS = datagen.draw_to_device(w, 0, w["ntrain"], self.dev)
+            T = datagen.draw(w, w["ntrain"], w["ntest"])
+        else:
+            S, T = datagen.make(w)
+            self.dS = mfsgd.samples_to_device(S, self.dev)
+        self.dT = mfsgd.samples_to_device(T, self.dev)
+        self.w = w
+        log(f"generated {workload}: {w['ntrain']} train + {w['ntest']} test in {time.perf_counter() - t0:.1f}s")
+
+    def setup(self, scheme, s, workers=0, partition=0):
+        """Initialise (and plan); returns the number of concurrent workers
+        (wavefronts) the launch will have, 0 for the library's default.
+        A wavefront-update grid of side s runs s teams of team_waves
+        wavefronts, grouped four to a workgroup (one-wavefront teams when
+        workers == s)."""
+        w, M = self.w, self.M
+        s = s or w.get("grid_s", 32)
+        team = 0
+        actual = workers
+        if scheme != "hogwild" and workers > 0:
+            team = max(1, workers // s)
+            actual = s if team == 1 else s * 4 * ((team + 3) // 4)
+        opts = dict(dtype=1 if w["dtype"] == "fp16" else 0, batch_f=256, workers=workers if scheme == "hogwild" else 0,
+                    depth=2, team_waves=team, partition=partition, debug=0)
+        for key, val in opts.items():
+            M.set_option(key, val)
+        M.init(w["m"], w["n"], w["k"], w["seed"])
+        if scheme != "hogwild":
+            M.plan(self.dS, s)
+        return actual
+
+    def epoch_ms(self, scheme, lr, lam):
+        torch, stream = self.torch, self.torch.cuda.current_stream()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        self.M.epoch(self.dS, lr, lam, lam, scheme, stream)
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b)
+
+
+def curves(args):
+    r = Runner(args.workload)
+    w = r.w
+    lr_t, lam = lr_schedule(w, args.lr)
+    rows = []
+    for scheme, s in parse_schemes(args.schemes):
+        r.setup(scheme, s, partition=args.partition)
+        s_eff = s or w.get("grid_s", 32)
+        elapsed, hist, hit = 0.0, [], None
+        for t in range(args.epochs):
+            ms = r.epoch_ms(scheme, lr_t(t), lam)
+            elapsed += ms
+            e = r.M.rmse(r.dT)
+            hist.append(e)
+            if hit is None and e <= args.target:
+                hit = (t + 1, elapsed)
+            print(json.dumps({"exp": "curves", "workload": w["name"], "lr": args.lr, "scheme": label(scheme, s_eff),
+                              "epoch": t + 1, "lr_t": round(lr_t(t), 6), "epoch_ms": round(ms, 3),
+                              "elapsed_ms": round(elapsed, 3), "test_rmse": round(e, 6)}), flush=True)
+        rows.append((label(scheme, s_eff), elapsed / args.epochs, hist, hit))
+        r.M.finalize()
+    marks = [t for t in (1, 2, 5, 10, 20, 40) if t <= args.epochs]
+    print(f"\n{w['name']}, lr schedule {args.lr}, {args.epochs} epochs, target test RMSE {args.target}\n")
+    print("| schedule | mean epoch ms | test RMSE after " + " / ".join(map(str, marks)) + " epochs | time to target |")
+    print("|---|---|---|---|")
+    for name, mean_ms, hist, hit in rows:
+        tt = f"{hit[1]:.0f} ms ({hit[0]} epochs)" if hit else "not reached"
+        print(f"| {name} | {mean_ms:.2f} | " + " / ".join(f"{hist[t - 1]:.4f}" for t in marks) + f" | {tt} |")
+
+
+def workers(args):
+    r = Runner(args.workload)
+    w = r.w
+    lr_t, lam = lr_schedule(w, "config")
+    counts = [int(x) for x in args.counts.split(",")]
+    table = {}
+    for scheme, s in parse_schemes(args.schemes):
+        s_eff = s or w.get("grid_s", 32)
+        for W in counts:
+            actual = r.setup(scheme, s, workers=W, partition=args.partition)
+            if actual != W:
+                log(f"{label(scheme, s_eff)}: {W} workers is not a team shape (runs {actual}); skipped")
+                r.M.finalize()
+                continue
+            resident = r.M.get_option("resident_waves")
+            if W == 0 and scheme == "hogwild":
+                W = resident
+            r.epoch_ms(scheme, lr_t(0), lam)
+            if scheme != "hogwild":
+                # workgroups per team as laid out (capped by the co-resident
+                # workgroups of the team's XCD); four wavefronts each, one for
+                # one-wavefront teams
+                _, sizes = r.M.debug_team_layout(s_eff)
+                actual = int(sizes.sum().item()) * (1 if W == s_eff else 4)
+                if actual != W:
+                    log(f"{label(scheme, s_eff)}: {W} workers requested, {actual} launched")
+                    W = actual
+            ms = min(r.epoch_ms(scheme, lr_t(1 + i), lam) for i in range(args.epochs))
+            ups = w["ntrain"] / (ms / 1e3)
+            table[(label(scheme, s_eff), W)] = ups
+            print(json.dumps({"exp": "workers", "workload": w["name"], "scheme": label(scheme, s_eff), "workers": W,
+                              "resident_waves": resident, "epoch_ms": round(ms, 3), "updates_per_s": ups}),
+                  flush=True)
+            r.M.finalize()
+    names = list(dict.fromkeys(k[0] for k in table))
+    print(f"\n{w['name']}: updates/s (10^9) of the epoch kernel against concurrent workers (wavefronts)\n")
+    print("| workers | " + " | ".join(names) + " |")
+    print("|---|" + "---|" * len(names))
+    for W in sorted({k[1] for k in table}):
+        print(f"| {W} | " + " | ".join(f"{table[(n, W)] / 1e9:.3f}" if (n, W) in table else "-" for n in names)
+              + " |")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("exp", choices=["curves", "workers"])
+    ap.add_argument("--workload", default="netflix_fp16")
+    ap.add_argument("--epochs", type=int, default=0, help="curves: epochs (default 20); workers: timed epochs (default 2)")
+    ap.add_argument("--lr", choices=["config", "paper"], default="config")
+    ap.add_argument("--schemes", default="")
+    ap.add_argument("--target", type=float, default=0.92)
+    ap.add_argument("--partition", type=int, default=0,
+                    help="batch-Hogwild! form: 0 one address space, 1 XCD-partitioned, 2 automatic")
+    ap.add_argument("--counts", default="32,64,128,256,512,1024,2048,4096,8192")
+    args = ap.parse_args()
+    if args.exp == "curves":
+        args.epochs = args.epochs or 20
+        args.schemes = args.schemes or "hogwild,wavefront:8,wavefront:32"
+        curves(args)
+    else:
+        args.epochs = args.epochs or 2
+        args.schemes = args.schemes or "hogwild,wavefront:32"
+        workers(args)
+
+
+if __name__ == "__main__":
+    main()
