@@ -79,6 +79,10 @@ def lib():
         L.orc_epoch_wavefront.argtypes = [i64, i64, i32, C.c_int, vp, vp, vp, i64, f32, f32, f32, i32, u64,
                                           i64, C.c_int]
         L.orc_epoch_wavefront.restype = C.c_int
+        L.orc_table_order.argtypes = [u64, i64, vp, i64, vp]
+        L.orc_table_order.restype = C.c_int
+        L.orc_epoch_table.argtypes = [i64, i64, i32, C.c_int, vp, vp, vp, i64, f32, f32, f32, i32, u64, i64]
+        L.orc_epoch_table.restype = C.c_int
         L.orc_rmse.argtypes = [i32, C.c_int, vp, vp, vp, i64]
         L.orc_rmse.restype = f64
         L.orc_sq_errors.argtypes = [i32, C.c_int, vp, vp, vp, i64, vp]
@@ -165,6 +169,27 @@ def epoch_wavefront(P, Qt, S, lr, lambda_p, lambda_q, s, seed, t, balanced=False
                                    _ptr(S), len(S), lr, lambda_p, lambda_q, s, seed, t, int(bool(balanced)))
     if rc:
         raise MemoryError("oracle wavefront epoch failed")
+
+
+def table_order(seed: int, t: int, blocks) -> np.ndarray:
+    """Order in which a single worker takes the given blocks (ids ascending:
+    the non-empty blocks) from the global scheduling table in epoch t."""
+    blocks = np.ascontiguousarray(blocks, dtype=np.int64)
+    out = np.empty(max(len(blocks), 1), dtype=np.int64)
+    if lib().orc_table_order(seed, t, _ptr(blocks), len(blocks), _ptr(out)):
+        raise MemoryError
+    return out[:len(blocks)]
+
+
+def epoch_table(P, Qt, S, lr, lambda_p, lambda_q, s, seed, t):
+    """In place: one global-table epoch with a single worker (the non-empty
+    blocks of the equal-range s x s grid in table_order, array order inside
+    a block)."""
+    S = _samples(S)
+    rc = lib().orc_epoch_table(P.shape[0], Qt.shape[0], P.shape[1], _dtype_code(P), _ptr(P), _ptr(Qt), _ptr(S),
+                               len(S), lr, lambda_p, lambda_q, s, seed, t)
+    if rc:
+        raise MemoryError("oracle global-table epoch failed")
 
 
 def epoch_hogwild_omp(P, Qt, S, lr, lambda_p, lambda_q, f=256, nthreads=0) -> int:

@@ -428,6 +428,79 @@ int orc_epoch_wavefront(int64_t m, int64_t n, int32_t k, int dtype, void* P, voi
 }
 
 /* ------------------------------------------------------------------------ */
+/* Global scheduling table (section 3.2.1): LIBMF's policy, which the paper   */
+/* measures on a GPU ("LIBMF-GPU") as the baseline its two schedules replace. */
+/* R is cut into an s x s grid of blocks (equal index ranges, as above); one  */
+/* table, used by one worker at a time, records which row blocks and column   */
+/* blocks are in use, and a free worker is given an idle block that shares    */
+/* neither with a block in progress.                                          */
+/* Reading: an epoch takes every non-empty block exactly once, and among the  */
+/* blocks not yet taken the choice is random (LIBMF's least-updated-first    */
+/* rule, with random ties, reduces to this inside one epoch).  The table keeps */
+/* the blocks not yet taken in a list, initially the non-empty block ids in   */
+/* ascending order.  Decision d of epoch t draws a position uniformly from    */
+/* the list (output d of stream (seed, TABLE + t), high 32 bits times the     */
+/* list length, shifted down 32), takes the first block at or cyclically     */
+/* after that position whose row and column are free, and moves the list's   */
+/* last entry into its place.  A single worker finds every block free, so    */
+/* its order is the draw order alone, which is what is computed here.        */
+/* ------------------------------------------------------------------------ */
+
+#define ORC_TAG_TABLE (1ULL << 40) /* + t for epoch t */
+
+int orc_table_order(uint64_t seed, int64_t t, const int64_t* blocks, int64_t nblocks, int64_t* order)
+{
+    int64_t* list = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nblocks > 0 ? nblocks : 1));
+    if (!list)
+        return -2;
+    memcpy(list, blocks, sizeof(int64_t) * (size_t)nblocks);
+    uint64_t stream = orc_stream(seed, ORC_TAG_TABLE + (uint64_t)t);
+    int64_t rem = nblocks;
+    for (int64_t d = 0; d < nblocks; d++) {
+        uint64_t x = orc_splitmix64(stream, (uint64_t)d);
+        int64_t pos = (int64_t)(((x >> 32) * (uint64_t)rem) >> 32);
+        order[d] = list[pos];
+        list[pos] = list[rem - 1];
+        rem--;
+    }
+    free(list);
+    return 0;
+}
+
+/* One epoch under the global table with a single worker: the non-empty blocks
+ * of the equal-range s x s grid in the order of orc_table_order, each block's
+ * samples in array order. */
+int orc_epoch_table(int64_t m, int64_t n, int32_t k, int dtype, void* P, void* Qt, const orc_sample* S,
+                    int64_t nnz, float lr, float lambda_p, float lambda_q, int32_t s, uint64_t seed, int64_t t)
+{
+    int64_t nb = (int64_t)s * s;
+    int64_t* order = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nnz > 0 ? nnz : 1));
+    int64_t* start = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nb + 1));
+    int64_t* blocks = (int64_t*)malloc(sizeof(int64_t) * (size_t)nb);
+    int64_t* seq = (int64_t*)malloc(sizeof(int64_t) * (size_t)nb);
+    double* buf = (double*)malloc(2 * sizeof(double) * (size_t)k);
+    int rc = -2;
+    if (order && start && blocks && seq && buf && orc_block_order(S, nnz, m, n, s, NULL, NULL, order, start) == 0) {
+        int64_t used = 0;
+        for (int64_t b = 0; b < nb; b++)
+            if (start[b + 1] > start[b])
+                blocks[used++] = b;
+        if (orc_table_order(seed, t, blocks, used, seq) == 0) {
+            for (int64_t d = 0; d < used; d++)
+                for (int64_t x = start[seq[d]]; x < start[seq[d] + 1]; x++)
+                    orc_update_sample(P, Qt, dtype, k, &S[order[x]], lr, lambda_p, lambda_q, buf, buf + k);
+            rc = 0;
+        }
+    }
+    free(order);
+    free(start);
+    free(blocks);
+    free(seq);
+    free(buf);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Test RMSE: the square root of the mean squared prediction error over the  */
 /* held-out samples (the convergence measure of section 3.2.4), without any  */
 /* clamping of the prediction.  ntest == 0 gives 0.                           */

@@ -421,3 +421,100 @@ def test_init_rows_equal_full_init(orc, dtype):
     rows = np.array([0, 299, 17, 17, 150])
     assert np.array_equal(orc.init_rows(300, 24, 31, 0, rows, dtype), P[rows])
     assert np.array_equal(orc.init_rows(70, 24, 31, 1, [69, 0, 5], dtype), Q[[69, 0, 5]])
+
+
+# ---------------------------------------------------------------------------- global scheduling table
+def test_table_order_is_a_permutation(orc):
+    rng = np.random.default_rng(21)
+    for nb in (0, 1, 2, 7, 100, 4096):
+        blocks = np.sort(rng.choice(1 << 20, size=nb, replace=False))
+        for t in (0, 5):
+            o = orc.table_order(99, t, blocks)
+            assert sorted(o.tolist()) == blocks.tolist()
+
+
+def test_table_order_is_uniform(orc):
+    """All 4! orders of four blocks appear equally often over the epochs (a draw
+    over the full list instead of the blocks left, or a taken block not replaced
+    by the list's last entry, repeats blocks or skews the orders)."""
+    counts = {}
+    N = 48000
+    for t in range(N):
+        key = tuple(orc.table_order(5150, t, [3, 9, 10, 17]).tolist())
+        counts[key] = counts.get(key, 0) + 1
+    assert len(counts) == 24
+    for c in counts.values():
+        assert abs(c - N / 24) < 5 * math.sqrt(N / 24)
+
+
+def test_table_order_keyed_by_seed_and_epoch(orc):
+    b = np.arange(50) * 3
+    a0 = orc.table_order(1, 0, b)
+    assert np.array_equal(a0, orc.table_order(1, 0, b))
+    assert not np.array_equal(a0, orc.table_order(1, 1, b))
+    assert not np.array_equal(a0, orc.table_order(2, 0, b))
+    assert not np.array_equal(a0, b)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_table_single_block_is_serial(orc, dtype):
+    rng = np.random.default_rng(13)
+    S = samples([(rng.integers(20), rng.integers(10), rng.normal()) for _ in range(400)], orc)
+    P, Q = orc.init_factors(20, 10, 4, 5, dtype)
+    P1, Q1, P2, Q2 = P.copy(), Q.copy(), P.copy(), Q.copy()
+    orc.epoch_table(P1, Q1, S, 0.05, 0.01, 0.02, 1, 5, 3)
+    orc.epoch_serial(P2, Q2, S, 0.05, 0.01, 0.02)
+    assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_table_diagonal_blocks_commute(orc, dtype):
+    """Samples only in the diagonal blocks (i, i): such blocks share no row and no
+    column (independent samples, section 2.3), so in whatever order the table
+    hands them out the epoch equals the serial epoch in array order."""
+    rng = np.random.default_rng(14)
+    m, n, k, s = 60, 45, 6, 5
+    rows = []
+    for x in range(2500):
+        u = int(rng.integers(m))
+        i = u * s // m
+        lo, hi = -(-i * n // s), -(-(i + 1) * n // s)
+        rows.append((u, int(rng.integers(lo, hi)), rng.uniform(1, 5)))
+    S = samples(rows, orc)
+    assert all(orc.row_block(x["u"], m, s) == orc.col_block(x["v"], n, s) for x in S)
+    P, Q = orc.init_factors(m, n, k, 8, dtype)
+    Ps, Qs = P.copy(), Q.copy()
+    orc.epoch_serial(Ps, Qs, S, 0.03, 0.05, 0.04)
+    for t in range(4):
+        Pt, Qt = P.copy(), Q.copy()
+        orc.epoch_table(Pt, Qt, S, 0.03, 0.05, 0.04, s, 8, t)
+        assert np.array_equal(Pt, Ps) and np.array_equal(Qt, Qs)
+
+
+def test_table_epoch_is_serial_over_its_schedule(orc):
+    """Blocks in the table's order, each block's samples in array order (the
+    stable bucketing pinned above), every sample exactly once."""
+    rng = np.random.default_rng(15)
+    m, n, k, s, seed, t = 70, 33, 5, 6, 41, 2
+    S = samples([(rng.integers(m), rng.integers(n), rng.uniform(1, 5)) for _ in range(1500)], orc)
+    order, start = orc.block_order(S, m, n, s)
+    nonempty = [b for b in range(s * s) if start[b + 1] > start[b]]
+    seq = np.concatenate([order[start[b]:start[b + 1]] for b in orc.table_order(seed, t, nonempty)])
+    assert sorted(seq.tolist()) == list(range(len(S)))
+    P, Q = orc.init_factors(m, n, k, seed, np.float32)
+    P1, Q1, P2, Q2 = P.copy(), Q.copy(), P.copy(), Q.copy()
+    orc.epoch_table(P1, Q1, S, 0.02, 0.05, 0.05, s, seed, t)
+    orc.epoch_serial(P2, Q2, S[seq], 0.02, 0.05, 0.05)
+    assert np.array_equal(P1, P2) and np.array_equal(Q1, Q2)
+    P3, Q3 = P.copy(), Q.copy()
+    orc.epoch_serial(P3, Q3, S, 0.02, 0.05, 0.05)
+    assert not np.array_equal(P1, P3)  # the block order does change the result
+
+
+def test_table_lr_zero_is_identity(orc):
+    rng = np.random.default_rng(16)
+    S = samples([(rng.integers(30), rng.integers(30), rng.normal()) for _ in range(600)], orc)
+    P, Q = orc.init_factors(30, 30, 8, 2, np.float16)
+    P1, Q1 = P.copy(), Q.copy()
+    orc.epoch_table(P1, Q1, S, 0.0, 0.05, 0.05, 4, 2, 0)
+    assert np.array_equal(P1, P) and np.array_equal(Q1, Q)
