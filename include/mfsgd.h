@@ -97,7 +97,25 @@ enum {
     /* the same schedule with one wavefront per worker and each block's
      * samples in their array order: the result then equals the serial
      * update in wave order up to floating-point rounding (deterministic). */
-    MFSGD_WAVEFRONT_DET = 2
+    MFSGD_WAVEFRONT_DET = 2,
+    /* LIBMF's global scheduling table (section 3.2.1), the baseline the two
+     * schedules above replace ("LIBMF-GPU" in the paper).  R is cut into a
+     * "table_grid" x "table_grid" grid of equal index ranges
+     * (floor(u*s/m), floor(v*s/n); planned internally, synchronously, on the
+     * first such epoch on a sample array).  Each of "table_workers"
+     * wavefronts is one worker: it takes a lock on the one table, picks a
+     * block not yet taken in this epoch whose row block and column block no
+     * other worker holds, marks both, releases the lock, updates the block's
+     * samples serially in array order, then clears its marks.  Every
+     * non-empty block is taken once per epoch.  The choice among the free
+     * blocks is random: the blocks not yet taken form a list (initially the
+     * non-empty block ids, ascending); decision d of epoch t draws a list
+     * position from output d of the SplitMix64 stream keyed (seed, 2^40 + t)
+     * (high 32 bits times the list length, shifted down 32), takes the first
+     * free block at or cyclically after it, and moves the list's last entry
+     * into its slot.  With one worker the result therefore equals the
+     * serial update in that block order (deterministic).  Needs nnz < 2^32. */
+    MFSGD_GLOBAL_TABLE = 3
 };
 
 enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
@@ -166,6 +184,11 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *   "stage_samples" samples per chunk of mfsgd_epoch_staged (default 2^25,
  *                  402 MB per buffer; three device buffers, and three
  *                  pinned host buffers for pageable arrays).
+ *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
+ *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
+ *                  table_grid / 2 (at least 1): about twice as many row and
+ *                  column blocks as workers, so that a free worker usually
+ *                  finds an idle block.
  *   "debug"        bit 0: count visits of every sample (read with
  *                  mfsgd_debug_read(MFSGD_DBG_VISITS)); bit 1: record the
  *                  schedule (MFSGD_DBG_TRACE).  Costs one extra atomic per
@@ -175,6 +198,7 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs the
  * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
  * "partitioned" (whether batch-Hogwild! runs partitioned for this model),
+ * "table_blocks" (non-empty blocks of the last global-table plan, 0 before one),
  * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
  * block-scheduled kernel), "teams_grid" (workgroups of the last
  * block-scheduled epoch, 0 before one).
@@ -205,13 +229,14 @@ int mfsgd_plan(const mfsgd_sample* samples, int64_t nnz, int32_t s, void* stream
 /* One epoch: every one of the nnz samples is used for exactly one update
  * (section 2.3), under `scheme`, with learning rate lr and regularisation
  * lambda_p, lambda_q (section 2.2).  Asynchronous on `stream`, except that
- * the first partitioned batch-Hogwild! epoch on a sample array plans it
- * (synchronously, like mfsgd_plan).  Increments the epoch counter, which
+ * the first partitioned batch-Hogwild! or global-table epoch on a sample
+ * array plans it (synchronously, like mfsgd_plan).  Increments the epoch counter, which
  * keys the per-epoch column orders.  Indices are not checked by the
  * one-address-space batch-Hogwild! (use mfsgd_check_samples): an index out
  * of range is undefined behaviour there.
  * EINVAL: nnz < 0, NULL samples with nnz > 0, unknown scheme, non-finite lr
- * or lambda, or (planning) an index out of range.  ESTATE: no init, or a
+ * or lambda, (planning) an index out of range, or nnz >= 2^32 for
+ * MFSGD_GLOBAL_TABLE.  ESTATE: no init, or a
  * wavefront scheme without a plan for these samples. */
 int mfsgd_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lambda_p, float lambda_q,
                 int32_t scheme, void* stream);
@@ -274,7 +299,13 @@ int64_t mfsgd_get_epoch(void);
  *                      caller's array).
  *   MFSGD_DBG_TRACE  : batch-Hogwild!: dst int32[ceil(nnz/f)], the worker
  *                      that ran each batch; wavefront: dst int32[s*s],
- *                      entry i*s+w = column block of worker i in wave w.
+ *                      entry i*s+w = column block of worker i in wave w;
+ *                      global table: dst int32[3*B], B = "table_blocks": for
+ *                      decision d, entry 3d = the block id I*s+J taken, 3d+1
+ *                      and 3d+2 = the values of one event counter when the
+ *                      block was taken and when it was given back (a block
+ *                      that shares a row or column block with another is
+ *                      taken only after the other was given back).
  *   MFSGD_DBG_PLAN_STARTS : the wavefront-update plan of the last mfsgd_plan:
  *                      count = s*s+1, dst int64 -- first planned position of
  *                      block (I, J) at entry I*s+J, nnz at entry s*s.
@@ -287,6 +318,12 @@ int64_t mfsgd_get_epoch(void);
  *                      each workgroup, -1 for an idle one.
  *   MFSGD_DBG_TEAM_SIZES : same layout, count = s, dst int32 -- workgroups
  *                      of each team.
+ *   MFSGD_DBG_TABLE_STARTS : the global-table plan: count = s*s+1 (s =
+ *                      "table_grid" of the plan), dst int64 -- first planned
+ *                      position of block (I, J) at entry I*s+J, nnz at s*s.
+ *   MFSGD_DBG_TABLE_ORDER  : same plan, count <= nnz, dst int64 -- position in
+ *                      the caller's array of each planned sample (needs a plan
+ *                      made while debug bit 0 was set).
  * dst may be host or device memory. */
 enum {
     MFSGD_DBG_VISITS = 1,
@@ -294,7 +331,9 @@ enum {
     MFSGD_DBG_PLAN_STARTS = 3,
     MFSGD_DBG_PLAN_ORDER = 4,
     MFSGD_DBG_TEAM_MAP = 5,
-    MFSGD_DBG_TEAM_SIZES = 6
+    MFSGD_DBG_TEAM_SIZES = 6,
+    MFSGD_DBG_TABLE_STARTS = 7,
+    MFSGD_DBG_TABLE_ORDER = 8
 };
 int mfsgd_debug_read(int32_t what, void* dst, int64_t count, void* stream);
 

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmfsgd.so")
-SOURCES = ["mfsgd_api.hip", "mfsgd_aux.hip", "mfsgd_kernels_f32.hip", "mfsgd_kernels_f16.hip"]
+SOURCES = ["mfsgd_api.hip", "mfsgd_aux.hip", "mfsgd_table.hip", "mfsgd_kernels_f32.hip", "mfsgd_kernels_f16.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -32,6 +32,8 @@ struct Options {
     int64_t spin_limit = int64_t(1) << 24;
     int64_t skip_stores = 2;
     int64_t stage_samples = int64_t(1) << 25;
+    int64_t table_grid = 256;
+    int64_t table_workers = 0;
     int64_t debug = 0;
 };
 
@@ -60,6 +62,27 @@ struct Plan {
     }
 };
 
+// The grouping of one sample array into the blocks of the global scheduling
+// table's grid (equal index ranges), and the table's device state.
+struct TablePlan {
+    const mfsgd_sample* src = nullptr;
+    int64_t nnz = -1;
+    int s = 0;
+    bool has_orig = false;
+    Sample* Sp = nullptr;
+    int64_t Sp_cap = 0;
+    int64_t* orig = nullptr;
+    int64_t orig_cap = 0;
+    int64_t* bstart = nullptr;
+    int64_t bstart_cap = 0;
+    uint32_t* blist = nullptr; // the non-empty blocks, ascending
+    int64_t blist_cap = 0;
+    uint32_t nb = 0;
+    uint32_t* tab = nullptr; // lock, counters, row/column marks, list (kTableHdr + 2 s + nb words)
+    int64_t tab_cap = 0;
+    bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
+};
+
 struct Context {
     bool inited = false;
     int device = 0;
@@ -81,6 +104,7 @@ struct Context {
     int* hflag = nullptr;   // pinned
     Plan wf;                // the caller's wavefront-update plan (mfsgd_plan)
     Plan hw;                // internal plan of the XCD-partitioned batch-Hogwild!
+    TablePlan gt;           // internal plan of the global scheduling table
     // planner scratch
     int64_t* counts = nullptr;
     int64_t counts_cap = 0;
@@ -193,6 +217,16 @@ void free_plan(Plan& p)
     p = Plan();
 }
 
+void free_table_plan(TablePlan& p)
+{
+    dfree(p.Sp);
+    dfree(p.orig);
+    dfree(p.bstart);
+    dfree(p.blist);
+    dfree(p.tab);
+    p = TablePlan();
+}
+
 void release_all()
 {
     Context& c = g;
@@ -210,6 +244,7 @@ void release_all()
         (void)hipHostFree(c.hflag);
     free_plan(c.wf);
     free_plan(c.hw);
+    free_table_plan(c.gt);
     dfree(c.counts);
     dfree(c.totals);
     dfree(c.bnd);
@@ -335,6 +370,8 @@ const OptSpec kOpts[] = {
     {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
     {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
     {"stage_samples", &Options::stage_samples, 64, int64_t(1) << 31, "stage_samples must be in [64, 2^31]"},
+    {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
+    {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
 };
 
@@ -369,7 +406,7 @@ int get_option_impl(const char* key, int64_t* value)
         }
     const bool ro = !std::strcmp(key, "resident_waves") || !std::strcmp(key, "xcds") || !std::strcmp(key, "cus") ||
                     !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
-                    !std::strcmp(key, "teams_grid");
+                    !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
@@ -384,6 +421,8 @@ int get_option_impl(const char* key, int64_t* value)
         *value = partitioned_hogwild() ? 1 : 0;
     else if (!std::strcmp(key, "teams_grid"))
         *value = g.lay_plan ? g.lay_grid : 0;
+    else if (!std::strcmp(key, "table_blocks"))
+        *value = g.gt.nnz >= 0 ? (int64_t)g.gt.nb : 0;
     else
         *value = g.cus;
     return MFSGD_OK;
@@ -625,6 +664,142 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     return MFSGD_OK;
 }
 
+// Group the samples by block of the table's s x s grid (equal index ranges),
+// keep the non-empty block list, size the table.  Synchronous.
+int build_table_plan(TablePlan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool keep_orig, hipStream_t st)
+{
+    Context& c = g;
+    pl.src = nullptr;
+    pl.nnz = -1;
+    const int64_t nblocks = (int64_t)s * s;
+    CHK(grow(&pl.Sp, &pl.Sp_cap, nnz, "table samples"));
+    if (keep_orig)
+        CHK(grow(&pl.orig, &pl.orig_cap, nnz, "table positions"));
+    CHK(grow(&pl.bstart, &pl.bstart_cap, nblocks + 1, "table block starts"));
+    TablePlanBuffers b{};
+    b.bstart = pl.bstart;
+    b.Sp = pl.Sp;
+    b.orig = keep_orig ? pl.orig : nullptr;
+    b.bad = c.bad;
+    // sort scratch, released again below
+    std::vector<void*> scratch;
+    auto take = [&](void** p, size_t bytes, const char* what) {
+        int rc = dalloc(p, bytes, what);
+        if (rc == MFSGD_OK)
+            scratch.push_back(*p);
+        return rc;
+    };
+    auto drop = [&]() {
+        for (void* p : scratch)
+            dfree(p);
+        scratch.clear();
+    };
+    int rc = MFSGD_OK;
+    const size_t words = sizeof(uint32_t) * (size_t)std::max<int64_t>(nnz, 1);
+    b.temp_bytes = table_sort_bytes(nnz, s);
+    if (nnz > 0 && b.temp_bytes == 0)
+        rc = fail(MFSGD_EHIP, "radix sort size query failed");
+    for (int i = 0; rc == MFSGD_OK && i < 2; ++i) {
+        rc = take((void**)&b.keys[i], words, "table sort keys");
+        if (rc == MFSGD_OK)
+            rc = take((void**)&b.vals[i], words, "table sort values");
+    }
+    if (rc == MFSGD_OK)
+        rc = take(&b.temp, b.temp_bytes, "table sort scratch");
+    hipError_t e = hipSuccess;
+    if (rc == MFSGD_OK) {
+        e = hipMemsetAsync(c.bad, 0, sizeof(int), st);
+        if (e == hipSuccess)
+            e = table_plan_build((const Sample*)samples, nnz, c.m, c.n, s, b, st);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(st);
+        if (e == hipSuccess && *c.hflag) {
+            *c.hflag = 0;
+            rc = bad_index_error();
+        } else if (e == hipSuccess) {
+            e = table_plan_gather((const Sample*)samples, nnz, b, st);
+            if (e == hipSuccess)
+                e = hipStreamSynchronize(st);
+        }
+        if (e != hipSuccess)
+            rc = fail(MFSGD_EHIP, std::string("table plan: ") + hipGetErrorString(e));
+    }
+    drop();
+    if (rc != MFSGD_OK)
+        return rc;
+    std::vector<int64_t> hstart((size_t)nblocks + 1);
+    HIPCHK(hipMemcpy(hstart.data(), pl.bstart, sizeof(int64_t) * hstart.size(), hipMemcpyDeviceToHost));
+    std::vector<uint32_t> blist;
+    for (int64_t x = 0; x < nblocks; ++x)
+        if (hstart[(size_t)x + 1] > hstart[(size_t)x])
+            blist.push_back((uint32_t)x);
+    CHK(grow(&pl.blist, &pl.blist_cap, (int64_t)blist.size(), "table block list"));
+    if (!blist.empty())
+        HIPCHK(hipMemcpy(pl.blist, blist.data(), sizeof(uint32_t) * blist.size(), hipMemcpyHostToDevice));
+    CHK(grow(&pl.tab, &pl.tab_cap, kTableHdr + 2 * (int64_t)s + (int64_t)blist.size(), "scheduling table"));
+    pl.nb = (uint32_t)blist.size();
+    pl.src = samples;
+    pl.nnz = nnz;
+    pl.s = s;
+    pl.has_orig = keep_orig;
+    return MFSGD_OK;
+}
+
+// One epoch under the global scheduling table (see k_table).
+int table_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, float lq, hipStream_t st)
+{
+    Context& c = g;
+    const int64_t dbg = g_opt.debug;
+    if (nnz >= (int64_t(1) << 32))
+        return fail(MFSGD_EINVAL, "the global scheduling table handles fewer than 2^32 samples");
+    const int s = (int)g_opt.table_grid;
+    const bool keep = (dbg & 1) != 0;
+    TablePlan& pl = c.gt;
+    if (!pl.matches(samples, nnz) || pl.s != s || (keep && !pl.has_orig))
+        CHK(build_table_plan(pl, samples, nnz, s, keep, st));
+    TableLaunch a{};
+    a.KP = c.KP;
+    a.depth = (int)g_opt.depth;
+    a.Sp = pl.Sp;
+    a.bstart = pl.bstart;
+    a.s = s;
+    a.nb = pl.nb;
+    a.draw = sm64_at(c.seed, kTagTable + (uint64_t)c.epoch);
+    a.P = c.P;
+    a.Q = c.Q;
+    a.lr = lr;
+    a.lp = lp;
+    a.lq = lq;
+    a.f = (int)g_opt.batch_f;
+    a.W = g_opt.table_workers > 0 ? g_opt.table_workers : std::max(1, s / 2);
+    a.tab = pl.tab;
+    a.spin_limit = (uint32_t)g_opt.spin_limit;
+    a.err = c.err;
+    if (dbg & 1) {
+        CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
+        c.visits_n = nnz;
+        HIPCHK(hipMemsetAsync(c.visits, 0, sizeof(uint32_t) * (size_t)(nnz > 0 ? nnz : 1), st));
+        a.visits = c.visits;
+        a.orig = pl.orig;
+    }
+    if (dbg & 2) {
+        const int64_t words = 3 * (int64_t)pl.nb;
+        CHK(grow(&c.trace, &c.trace_cap, words, "trace"));
+        c.trace_n = words;
+        HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)(words > 0 ? words : 1), st));
+        a.trace = c.trace;
+    }
+    HIPCHK(table_reset(pl.tab, pl.blist, pl.nb, s, st));
+    if (c.dtype == MFSGD_FP16)
+        HIPCHK(table_epoch_f16(a, st));
+    else
+        HIPCHK(table_epoch_f32(a, st));
+    c.epoch += 1;
+    return MFSGD_OK;
+}
+
 int plan_impl(const mfsgd_sample* samples, int64_t nnz, int32_t s, hipStream_t st)
 {
     if (!g.inited)
@@ -827,8 +1002,11 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         return fail(MFSGD_EINVAL, "bad sample array");
     if (!std::isfinite(lr) || !std::isfinite(lp) || !std::isfinite(lq))
         return fail(MFSGD_EINVAL, "lr and lambdas must be finite");
-    if (scheme != MFSGD_BATCH_HOGWILD && scheme != MFSGD_WAVEFRONT && scheme != MFSGD_WAVEFRONT_DET)
+    if (scheme != MFSGD_BATCH_HOGWILD && scheme != MFSGD_WAVEFRONT && scheme != MFSGD_WAVEFRONT_DET &&
+        scheme != MFSGD_GLOBAL_TABLE)
         return fail(MFSGD_EINVAL, "unknown scheme");
+    if (scheme == MFSGD_GLOBAL_TABLE)
+        return table_epoch(samples, nnz, lr, lp, lq, st);
     const int64_t dbg = g_opt.debug;
     const bool hog = scheme == MFSGD_BATCH_HOGWILD;
     const bool blocked = !hog || partitioned_hogwild();
@@ -1141,6 +1319,15 @@ int debug_read_impl(int32_t what, void* dst, int64_t count, hipStream_t st)
             return fail(MFSGD_ESTATE, "no wavefront plan with positions (plan with debug bit 0 set)");
         if (count)
             HIPCHK(hipMemcpyAsync(dst, c.wf.orig, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_TABLE_STARTS) {
+        if (c.gt.nnz < 0 || count != (int64_t)c.gt.s * c.gt.s + 1)
+            return fail(MFSGD_ESTATE, "no global-table plan, or count is not s*s+1");
+        HIPCHK(hipMemcpyAsync(dst, c.gt.bstart, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_TABLE_ORDER) {
+        if (c.gt.nnz < 0 || !c.gt.has_orig || count > c.gt.nnz)
+            return fail(MFSGD_ESTATE, "no global-table plan with positions (run it with debug bit 0 set)");
+        if (count)
+            HIPCHK(hipMemcpyAsync(dst, c.gt.orig, sizeof(int64_t) * (size_t)count, hipMemcpyDefault, st));
     } else if (what == MFSGD_DBG_TEAM_MAP || what == MFSGD_DBG_TEAM_SIZES) {
         if (!c.lay_plan)
             return fail(MFSGD_ESTATE, "no block-scheduled epoch has run");

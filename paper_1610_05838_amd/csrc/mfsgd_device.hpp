@@ -173,6 +173,8 @@ __host__ __device__ __forceinline__ uint64_t sm64_at(uint64_t s0, uint64_t i)
 // Stream keys used by the library: stream `tag` is output `tag` of the
 // generator seeded with the user seed.
 enum : uint64_t { kTagP = 1, kTagQ = 2, kTagColPerm = 16, kTagWaveOffset = 17 };
+// global scheduling table: the draws of epoch t come from stream kTagTable + t
+constexpr uint64_t kTagTable = uint64_t(1) << 40;
 
 // Durstenfeld shuffle of 0..s-1: step i (from s-1 down to 1) swaps a[i]
 // with a[j], j = high 32 bits of draw (s-1-i) times (i+1), shifted down 32.

@@ -195,6 +195,152 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     }
 }
 
+// LIBMF's global scheduling table (section 3.2.1), the baseline that
+// batch-Hogwild! and wavefront-update replace.  R is cut into an s x s grid;
+// every wavefront is one worker; a free worker takes the table's lock, picks
+// a block not yet taken this epoch whose row block and column block are both
+// unused, marks them used, releases the lock and updates the block's samples
+// serially; then it clears its two marks.  An epoch takes every non-empty
+// block once.
+//
+// The blocks not yet taken form a list.  Decision d draws a list position
+// from output d of this epoch's stream (high 32 bits times the list length,
+// shifted down 32); the holder of the lock checks 64 consecutive list entries
+// (cyclically from that position) per step, one per lane, takes the first
+// whose row and column are unused and moves the list's last entry into its
+// slot.  A single worker therefore takes the blocks in the draw order alone.
+//
+// Every table word is read and written with agent-scope atomics, which all
+// XCDs see coherently; the writes made under the lock have completed
+// (s_waitcnt) before the lock is released.  The block's rows are handed over
+// between XCDs as in the block-scheduled kernel: the worker writes its L2
+// back (agent-scope release) before it clears its marks, and a worker that
+// has taken a block invalidates its caches (agent-scope acquire) before it
+// reads the rows.
+//
+// Nothing waits for a particular wavefront, and no wavefront leaves while it
+// holds the lock or a block; a worker that finds the lock taken or no block
+// free polls (with a sleep), and after spin_limit polls in a row raises *err,
+// upon which every worker leaves at its next visit to the table.
+template <int KP, typename T, int D, bool DBG>
+__global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
+                                              int s, uint32_t nb, uint64_t draw, T* __restrict__ P,
+                                              T* __restrict__ Q, float lr, float lp, float lq, int f, uint32_t* tab,
+                                              uint32_t spin_limit, int* err, DebugSink dbg, int32_t* trace)
+{
+    const int lane = lane_id();
+    uint32_t* const lock = tab;
+    uint32_t* const left = tab + 1;
+    uint32_t* const events = tab + 2;
+    uint32_t* const row_used = tab + kTableHdr;
+    uint32_t* const col_used = row_used + s;
+    uint32_t* const list = col_used + s;
+    const uint32_t us = (uint32_t)s;
+    uint32_t polls = 0;
+    for (;;) {
+        // take the lock (test, then test-and-set)
+        int got = 0, stop = 0;
+        if (lane == 0) {
+            stop = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+            if (!stop && __hip_atomic_load(lock, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+                uint32_t expect = 0u;
+                got = __hip_atomic_compare_exchange_strong(lock, &expect, 1u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (__builtin_amdgcn_readfirstlane(stop))
+            return;
+        bool wait = !__builtin_amdgcn_readfirstlane(got);
+        uint32_t fpos = 0, fblk = 0, d = 0;
+        if (!wait) {
+            uint32_t rem = 0;
+            if (lane == 0)
+                rem = __hip_atomic_load(left, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            rem = __builtin_amdgcn_readfirstlane(rem);
+            if (rem == 0u) {
+                if (lane == 0)
+                    __hip_atomic_store(lock, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return; // every block has been taken
+            }
+            d = nb - rem;
+            const uint64_t x = sm64_at(draw, (uint64_t)d);
+            const uint32_t pos0 = (uint32_t)(((x >> 32) * (uint64_t)rem) >> 32);
+            bool found = false;
+            for (uint32_t j0 = 0; j0 < rem && !found; j0 += 64) {
+                const uint32_t j = j0 + (uint32_t)lane;
+                bool ok = false;
+                uint32_t pos = 0, blk = 0;
+                if (j < rem) {
+                    pos = pos0 + j;
+                    pos = pos >= rem ? pos - rem : pos;
+                    blk = __hip_atomic_load(list + pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ok = __hip_atomic_load(row_used + blk / us, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u &&
+                         __hip_atomic_load(col_used + blk % us, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
+                }
+                const uint64_t hit = __builtin_amdgcn_ballot_w64(ok);
+                if (hit) {
+                    const int l = (int)__builtin_ctzll(hit);
+                    fpos = __builtin_amdgcn_readlane(pos, l);
+                    fblk = __builtin_amdgcn_readlane(blk, l);
+                    found = true;
+                }
+            }
+            if (lane == 0) {
+                if (found) {
+                    const uint32_t last = __hip_atomic_load(list + rem - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(list + fpos, last, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(left, rem - 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(row_used + fblk / us, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(col_used + fblk % us, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (DBG && trace) {
+                        const uint32_t stamp =
+                            __hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        trace[3 * (int64_t)d] = (int32_t)fblk;
+                        trace[3 * (int64_t)d + 1] = (int32_t)stamp;
+                    }
+                }
+                // every table write has completed before the lock is free
+                __builtin_amdgcn_s_waitcnt(0);
+                __hip_atomic_store(lock, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            wait = !found;
+        }
+        if (wait) {
+            int give_up = 0;
+            if (lane == 0 && ++polls > spin_limit) {
+                __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                give_up = 1;
+            }
+            if (__builtin_amdgcn_readfirstlane(give_up))
+                return;
+            __builtin_amdgcn_s_sleep(8);
+            continue;
+        }
+        polls = 0;
+        // rows of this block written on other XCDs become visible once this
+        // wavefront's caches are invalidated
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        const int64_t lo = bstart[fblk], hi = bstart[fblk + 1];
+        DebugSink blk = dbg;
+        blk.trace = nullptr;
+        if (blk.orig)
+            blk.orig += lo;
+        run_worker<KP, T, D, DBG, false>(Sp + lo, hi - lo, 1, 0, f, P, Q, lr, lp, lq, blk);
+        // the block's stores reach memory before its row and column are free
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (lane == 0) {
+            if (DBG && trace) {
+                trace[3 * (int64_t)d + 2] =
+                    (int32_t)__hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __builtin_amdgcn_s_waitcnt(0);
+            }
+            __hip_atomic_store(row_used + fblk / us, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(col_used + fblk % us, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
 template <int KP, typename T, int D>
 static int occupancy_blocked_t(int threads)
 {
@@ -342,6 +488,37 @@ static hipError_t launch_epoch_kp(const EpochLaunch& a, hipStream_t st)
 }
 
 template <int KP, typename T, int D>
+static hipError_t launch_table_t(const TableLaunch& a, hipStream_t st)
+{
+    if (a.nb == 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)a.W), block(64);
+    if (a.visits || a.trace) {
+        const DebugSink dbg{a.visits, a.orig, nullptr};
+        hipLaunchKernelGGL((k_table<KP, T, D, true>), grid, block, 0, st, a.Sp, a.bstart, a.s, a.nb, a.draw, (T*)a.P,
+                           (T*)a.Q, a.lr, a.lp, a.lq, a.f, a.tab, a.spin_limit, a.err, dbg, a.trace);
+    } else {
+        const DebugSink dbg{nullptr, nullptr, nullptr};
+        hipLaunchKernelGGL((k_table<KP, T, D, false>), grid, block, 0, st, a.Sp, a.bstart, a.s, a.nb, a.draw,
+                           (T*)a.P, (T*)a.Q, a.lr, a.lp, a.lq, a.f, a.tab, a.spin_limit, a.err, dbg,
+                           (int32_t*)nullptr);
+    }
+    return hipGetLastError();
+}
+
+template <int KP, typename T>
+static hipError_t launch_table_kp(const TableLaunch& a, hipStream_t st)
+{
+    switch (a.depth) {
+    case 1: return launch_table_t<KP, T, 1>(a, st);
+    case 2: return launch_table_t<KP, T, 2>(a, st);
+    case 4: return launch_table_t<KP, T, 4>(a, st);
+    case 8: return launch_table_t<KP, T, 8>(a, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int KP, typename T, int D>
 static int occupancy_t()
 {
     int blocks = 0;
@@ -388,6 +565,17 @@ struct Dispatch {
         case 128: return launch_epoch_kp<128, T>(a, st);
         case 256: return launch_epoch_kp<256, T>(a, st);
         case 512: return launch_epoch_kp<512, T>(a, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
+    static hipError_t table_epoch(const TableLaunch& a, hipStream_t st)
+    {
+        switch (a.KP) {
+        case 32: return launch_table_kp<32, T>(a, st);
+        case 64: return launch_table_kp<64, T>(a, st);
+        case 128: return launch_table_kp<128, T>(a, st);
+        case 256: return launch_table_kp<256, T>(a, st);
+        case 512: return launch_table_kp<512, T>(a, st);
         default: return hipErrorInvalidValue;
         }
     }

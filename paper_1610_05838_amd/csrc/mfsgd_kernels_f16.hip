@@ -5,6 +5,8 @@ namespace mfsgd {
 
 hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st) { return Dispatch<half_t>::epoch(a, st); }
 
+hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st) { return Dispatch<half_t>::table_epoch(a, st); }
+
 int occupancy_f16(int KP, int depth) { return Dispatch<half_t>::occupancy(KP, depth); }
 
 int occupancy_blocked_f16(int KP, int depth, int threads)

@@ -55,9 +55,40 @@ struct EpochLaunch {
     int32_t* trace_batch;
 };
 
+// Global scheduling table (LIBMF's policy, the baseline of section 3.2.1).
+// tab, in 32-bit words: [0] lock, [1] blocks not yet taken this epoch,
+// [2] event counter (debug stamps), [kTableHdr, +s) row block in use,
+// [kTableHdr + s, +s) column block in use, [kTableHdr + 2 s, + nb) the blocks
+// not yet taken.
+constexpr int kMaxTableGrid = 1024; // largest grid side of the table
+constexpr int kTableHdr = 64;
+
+struct TableLaunch {
+    int KP, depth;
+    const Sample* Sp;      // samples grouped by block
+    const int64_t* bstart; // s*s+1 block starts
+    int s;
+    uint32_t nb;           // non-empty blocks (entries of the list)
+    uint64_t draw;         // this epoch's stream of list positions
+    void* P;
+    void* Q;
+    float lr, lp, lq;
+    int f;
+    int64_t W;             // workers (one wavefront each)
+    uint32_t* tab;
+    uint32_t spin_limit;
+    int* err;
+    // debug
+    uint32_t* visits;
+    const int64_t* orig;
+    int32_t* trace;        // 3 per decision: block, claim stamp, release stamp
+};
+
 // Implemented per storage type in mfsgd_kernels_f32.hip / mfsgd_kernels_f16.hip.
 hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st);
 hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st);
+hipError_t table_epoch_f32(const TableLaunch& a, hipStream_t st);
+hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st);
 int occupancy_f32(int KP, int depth);
 int occupancy_f16(int KP, int depth);
 int occupancy_blocked_f32(int KP, int depth, int threads); // workgroups per CU
@@ -103,5 +134,28 @@ hipError_t plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s,
 // scatter into the planned copy (run only after plan_build reported no bad index)
 hipError_t plan_scatter(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const PlanBuffers& b,
                         hipStream_t st);
+
+// Global-table plan (mfsgd_table.hip): stable grouping of the samples by block
+// floor(u*s/m) * s + floor(v*s/n) for s up to kMaxTableGrid, through a radix
+// sort of (block id, position) pairs.  Needs nnz < 2^32.
+struct TablePlanBuffers {
+    uint32_t* keys[2]; // nnz each
+    uint32_t* vals[2]; // nnz each
+    void* temp;        // table_sort_bytes(nnz, s)
+    size_t temp_bytes;
+    int64_t* bstart;   // s*s+1
+    Sample* Sp;        // planned copy
+    int64_t* orig;     // planned position -> caller position (optional)
+    int* bad;          // index-range flag
+};
+size_t table_sort_bytes(int64_t nnz, int s);
+// keys, sort and block starts; raises *b.bad on an index out of range
+hipError_t table_plan_build(const Sample* S, int64_t nnz, int64_t m, int64_t n, int s, const TablePlanBuffers& b,
+                            hipStream_t st);
+// gather into the planned copy (run only after table_plan_build reported no bad index)
+hipError_t table_plan_gather(const Sample* S, int64_t nnz, const TablePlanBuffers& b, hipStream_t st);
+// table state at the start of an epoch: lock free, every flag clear, the list
+// = blist[0..nb) (the non-empty blocks, ascending)
+hipError_t table_reset(uint32_t* tab, const uint32_t* blist, uint32_t nb, int s, hipStream_t st);
 
 } // namespace mfsgd

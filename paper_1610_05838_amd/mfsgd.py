@@ -23,11 +23,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmfsgd.so")
 
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ETIMEOUT, ENUMERIC = 0, -1, -2, -3, -4, -5, -6
-BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET = 0, 1, 2
+BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET, GLOBAL_TABLE = 0, 1, 2, 3
 FP32, FP16 = 0, 1
 DBG_VISITS, DBG_TRACE, DBG_PLAN_STARTS, DBG_PLAN_ORDER, DBG_TEAM_MAP, DBG_TEAM_SIZES = 1, 2, 3, 4, 5, 6
+DBG_TABLE_STARTS, DBG_TABLE_ORDER = 7, 8
 
-SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET}
+SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET,
+           "table": GLOBAL_TABLE}
 
 SAMPLE_DTYPE = np.dtype([("u", "<i4"), ("v", "<i4"), ("r", "<f4")])
 
@@ -216,6 +218,20 @@ def debug_plan_starts(s: int, stream=None) -> torch.Tensor:
 def debug_plan_order(nnz: int, stream=None) -> torch.Tensor:
     out = torch.empty(max(nnz, 1), dtype=torch.int64, device="cuda")
     _check(lib().mfsgd_debug_read(DBG_PLAN_ORDER, C.c_void_p(out.data_ptr()), nnz, _stream(stream)),
+           "mfsgd_debug_read")
+    return out[:nnz]
+
+
+def debug_table_starts(s: int, stream=None) -> torch.Tensor:
+    out = torch.empty(s * s + 1, dtype=torch.int64, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_TABLE_STARTS, C.c_void_p(out.data_ptr()), s * s + 1, _stream(stream)),
+           "mfsgd_debug_read")
+    return out
+
+
+def debug_table_order(nnz: int, stream=None) -> torch.Tensor:
+    out = torch.empty(max(nnz, 1), dtype=torch.int64, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_TABLE_ORDER, C.c_void_p(out.data_ptr()), nnz, _stream(stream)),
            "mfsgd_debug_read")
     return out[:nnz]
 

@@ -1,0 +1,194 @@
+"""GPU parity of the global scheduling table (LIBMF's policy, section 3.2.1)
+through the C ABI, against the CPU oracle.
+
+* The table's grouping of the samples into blocks equals the oracle's stable
+  bucketing bit for bit (block starts and planned positions).
+* One worker takes the blocks in the oracle's table order (bit-exact trace) and
+  its factors match the oracle's single-worker epoch within max-abs 1e-4
+  (binary32) / 2e-2 (binary16).
+* Many workers: every sample is used once, every non-empty block is taken once,
+  and blocks that share a row block or a column block are never held at the
+  same time (claim/release stamps of one event counter); the test RMSE after 5
+  epochs is within 1e-3 (binary32) / 5e-3 (binary16) of the serial oracle's.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from test_gpu_parity import TOL, factors, maxabs, rand_samples, scaled_tiny, setup
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def M():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1610_05838_amd import mfsgd
+    mfsgd.lib()
+    yield mfsgd
+    mfsgd.finalize()
+
+
+def nonempty_blocks(S, m, n, s):
+    _, start = oracle.block_order(S, m, n, s)
+    return np.flatnonzero(np.diff(start) > 0)
+
+
+def zipf_samples(gen, m, n, nnz):
+    w = gen.workload("netflix", m=m, n=n, ntrain=nnz, ntest=0)
+    return w, gen.draw(w, 0, nnz)
+
+
+@pytest.mark.parametrize("s", [1, 7, 64, 256, 1024])
+def test_table_plan_is_the_oracles_bucketing(M, gen, s):
+    """Block starts and planned positions equal the oracle's stable bucketing;
+    an lr = 0 epoch with visit counting uses every sample once and changes
+    nothing."""
+    w, S = zipf_samples(gen, 30_000, 2_500, 200_003)
+    m, n = w["m"], w["n"]
+    setup(M, m, n, 32, 3, table_grid=s, table_workers=4, debug=1)
+    dS = M.samples_to_device(S)
+    P0, Q0 = factors(M, m, n, 32, np.float32)
+    M.epoch(dS, 0.0, 0.0, 0.0, "table")
+    order, start = oracle.block_order(S, m, n, s)
+    assert np.array_equal(M.debug_table_starts(s).cpu().numpy(), start)
+    assert np.array_equal(M.debug_table_order(len(S)).cpu().numpy(), order)
+    assert M.get_option("table_blocks") == int(np.count_nonzero(np.diff(start)))
+    assert np.all(M.debug_visits(len(S)).cpu().numpy() == 1)
+    P, Q = factors(M, m, n, 32, np.float32)
+    assert np.array_equal(P, P0) and np.array_equal(Q, Q0)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("s", [1, 3, 16, 64])
+def test_table_single_worker_matches_oracle(M, gen, dtype, s):
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, dtype, table_grid=s, table_workers=1, debug=2)
+    dS = M.samples_to_device(S)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    blocks = nonempty_blocks(S, m, n, s)
+    for t in range(2):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "table")
+        oracle.epoch_table(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, t)
+        tr = M.debug_trace(3 * len(blocks)).cpu().numpy().reshape(-1, 3)
+        assert np.array_equal(tr[:, 0], oracle.table_order(seed, t, blocks))
+        assert np.array_equal(tr[:, 1:].ravel(), np.arange(2 * len(blocks)))  # one block at a time
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("depth", [1, 8])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_table_single_worker_k128_zipf(M, gen, dtype, depth):
+    """k = 128 (one binary32 element pair per lane, or one binary16 pair), Zipf
+    rows: runs of one hot row inside a block, forwarded between the samples a
+    wavefront keeps in flight."""
+    w, S = zipf_samples(gen, 20_000, 3_000, 300_000)
+    m, n, k, seed, s = w["m"], w["n"], w["k"], w["seed"], 32
+    setup(M, m, n, k, seed, dtype, table_grid=s, table_workers=1, depth=depth)
+    dS = M.samples_to_device(S)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "table")
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    oracle.epoch_table(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, seed, 0)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("s,W", [(128, 64), (64, 200), (512, 256)])
+def test_table_concurrent_schedule_is_conflict_free(M, s, W):
+    """Many workers: each non-empty block taken once, each sample used once,
+    and no two blocks that share a row block or a column block held at once."""
+    rng = np.random.default_rng(s + W)
+    m, n = 40_000, 9_000
+    S = rand_samples(rng, m, n, 600_001)
+    setup(M, m, n, 32, 9, table_grid=s, table_workers=W, debug=3)
+    dS = M.samples_to_device(S)
+    blocks = nonempty_blocks(S, m, n, s)
+    B = len(blocks)
+    M.epoch(dS, 0.002, 0.01, 0.01, "table")
+    assert np.all(M.debug_visits(len(S)).cpu().numpy() == 1)
+    tr = M.debug_trace(3 * B).cpu().numpy().reshape(-1, 3).astype(np.int64)
+    assert np.array_equal(np.sort(tr[:, 0]), blocks)
+    assert np.array_equal(np.sort(tr[:, 1:].ravel()), np.arange(2 * B))
+    assert np.all(tr[:, 1] < tr[:, 2])
+    assert np.all(np.diff(tr[:, 1]) > 0)  # decisions are numbered in lock order
+    rb, cb = tr[:, 0] // s, tr[:, 0] % s
+    for key in (rb, cb):
+        o = np.lexsort((tr[:, 1], key))
+        same = key[o][1:] == key[o][:-1]
+        # within one row (column) block, each block is taken after the previous one was given back
+        assert np.all(tr[o, 1][1:][same] > tr[o, 2][:-1][same])
+    # workers did overlap: at some stamp more than one block was held
+    ev = np.zeros(2 * B, dtype=np.int64)
+    ev[tr[:, 1]] = 1
+    ev[tr[:, 2]] = -1
+    held = np.cumsum(ev).max()
+    print(f"s={s} W={W} blocks={B} most held at once={held}")
+    assert 1 < held <= min(W, s)
+
+
+@pytest.mark.parametrize("dtype,tol", [(np.float32, 1e-3), (np.float16, 5e-3)])
+def test_table_rmse_gap(M, gen, dtype, tol):
+    """32 workers on a 64 x 64 table (blocks of one epoch are independent while
+    held, so the gap comes from the block order alone): test RMSE after 5
+    epochs within tol of the serial oracle's."""
+    w, S, T = scaled_tiny(gen, 4)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, dtype, table_grid=64, table_workers=32)
+    dS, dT = M.samples_to_device(S), M.samples_to_device(T)
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    hist = []
+    for t in range(5):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "table")
+        oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
+        hist.append(M.rmse(dT))
+    want = oracle.rmse(Po, Qo, T)
+    print(f"table rmse {hist} oracle {want:.6f} gap={hist[-1] - want:+.6f}")
+    assert all(b < a for a, b in zip(hist, hist[1:]))
+    assert abs(hist[-1] - want) <= tol
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_table_lr_zero_is_identity(M, dtype):
+    rng = np.random.default_rng(5)
+    m, n, k = 3000, 1000, 64
+    S = rand_samples(rng, m, n, 150_000)
+    setup(M, m, n, k, 6, dtype, table_grid=100, table_workers=48)
+    P0, Q0 = factors(M, m, n, k, dtype)
+    M.epoch(M.samples_to_device(S), 0.0, 0.05, 0.05, "table")
+    P, Q = factors(M, m, n, k, dtype)
+    assert np.array_equal(P, P0) and np.array_equal(Q, Q0)
+
+
+def test_table_errors_and_timeout(M):
+    """Index errors at planning, empty arrays, re-planning when the grid
+    changes, and a host-forced spin limit: the waiting workers give up, every
+    worker leaves, the error surfaces at the next sync and the next epoch runs
+    normally."""
+    rng = np.random.default_rng(7)
+    m, n = 800, 800
+    setup(M, m, n, 32, 4, table_grid=2, table_workers=8, spin_limit=1)
+    bad = rand_samples(rng, m, n, 1000)
+    bad["u"][999] = m
+    with pytest.raises(M.MfsgdError) as e:
+        M.epoch(M.samples_to_device(bad), 0.01, 0.0, 0.0, "table")
+    assert e.value.code == M.EINVAL
+    S = rand_samples(rng, m, n, 400_000)
+    dS = M.samples_to_device(S)
+    M.epoch(dS[:0], 0.01, 0.0, 0.0, "table")
+    M.sync()
+    M.epoch(dS, 0.001, 0.0, 0.0, "table")
+    with pytest.raises(M.MfsgdError) as e:
+        M.sync()
+    assert e.value.code == M.ETIMEOUT
+    M.set_option("spin_limit", 1 << 24)
+    M.set_option("table_grid", 4)
+    M.set_option("debug", 1)
+    M.epoch(dS, 0.001, 0.0, 0.0, "table")
+    M.sync()
+    assert M.get_option("table_blocks") == 16
+    assert np.all(M.debug_visits(len(S)).cpu().numpy() == 1)
