@@ -114,7 +114,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="netflix")
-    ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det"])
+    ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det", "table"],
+                    help="table: the global scheduling table (LIBMF's policy; --set table_grid=S --set "
+                         "table_workers=W), planned in the first warm-up epoch")
     ap.add_argument("--grid-s", type=int, default=0, help="wavefront grid side (0: the workload's, else 32)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--depth", type=int, default=2)
@@ -182,7 +184,12 @@ def main():
     partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged
     kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
     grid_s = args.grid_s or w.get("grid_s", 32)
-    if args.scheme != "hogwild":
+    if args.scheme == "table":
+        kernel = "k_table"
+        grid_s = mfsgd.get_option("table_grid")
+        if args.warmup < 1:
+            raise SystemExit("--scheme table plans in its first epoch: use --warmup 1 or more")
+    elif args.scheme != "hogwild":
         t0 = time.perf_counter()
         mfsgd.plan(dS, grid_s)
         log(f"wavefront plan (s={grid_s}) {time.perf_counter() - t0:.3f}s")
@@ -266,6 +273,10 @@ def main():
         "epoch_updates_per_s": nnz / avg_epoch_s,
         "test_rmse": rmses[-1],
     }
+    if args.scheme == "table":
+        tw = mfsgd.get_option("table_workers")
+        out["config"]["workers"] = tw or max(1, grid_s // 2)
+        out["config"]["table_blocks"] = mfsgd.get_option("table_blocks")
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded prefix")
         serial, omp = cpu_baseline(w, S, args.cpu_seconds, args.cpu_threads)

@@ -124,9 +124,9 @@ def counter_per_dispatch(d, counter):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--workload", default="netflix")
-    ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det"])
-    ap.add_argument("--kernel", default="", help="epoch kernel name (default: whichever of k_hogwild and k_blocked "
-                                                 "takes more time in the trace)")
+    ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det", "table"])
+    ap.add_argument("--kernel", default="", help="epoch kernel name (default: whichever of k_hogwild, k_blocked "
+                                                 "and k_table takes more time in the trace)")
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--out", default="")
     ap.add_argument("--limit", type=int, default=400, help="seconds per rocprofv3 pass")
@@ -163,7 +163,7 @@ def main():
     kernel = a.kernel
     if not kernel:
         tot = {k: sum(float(r["TotalDurationNs"]) for r in stats if short(r["Name"]).split("<")[0].endswith(k))
-               for k in ("k_hogwild", "k_blocked")}
+               for k in ("k_hogwild", "k_blocked", "k_table")}
         kernel = max(tot, key=tot.get)
     tag = f"{kernel}_{a.workload}" + ("" if a.scheme == "hogwild" else f"_{a.scheme}")
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in trace

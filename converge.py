@@ -9,10 +9,14 @@ workers figures).
       which each schedule first reaches --target.
 
   python converge.py workers [--workload netflix_fp16] [--counts 64,128,...,8192]
-                             [--schemes hogwild,wavefront:32]
+                             [--schemes hogwild,wavefront:32,table] [--uniform]
       Updates/s of the epoch kernel against the number of concurrent workers
       (wavefronts), one warm-up and --epochs timed epochs per point; a count
-      of 0 is the library's default launch.
+      of 0 is the library's default launch.  "table" is the global scheduling
+      table (LIBMF's policy, section 3.2.1) on a grid of twice as many row and
+      column blocks as workers (at most 1024), "table:s" on a fixed grid of
+      side s.  --uniform draws the workload's users and items uniformly
+      instead of Zipf-like.
 
 Learning rates: "config" is the workload's own schedule (lr * decay^t);
 "paper" is the decaying schedule of the evaluation section,
@@ -64,20 +68,22 @@ def parse_schemes(text: str):
     out = []
     for item in text.split(","):
         name, _, s = item.partition(":")
-        if name not in ("hogwild", "wavefront", "wavefront_det"):
+        if name not in ("hogwild", "wavefront", "wavefront_det", "table"):
             raise SystemExit(f"unknown scheme {name!r}")
         out.append((name, int(s) if s else 0))
     return out
 
 
 def label(scheme, s):
+    if scheme == "table":
+        return "global table" + (f" s={s}" if s else " s=2W")
     return scheme if scheme == "hogwild" else f"{scheme} s={s}"
 
 
 class Runner:
     """Holds the device copies of one workload's train and test sets."""
 
-    def __init__(self, workload: str):
+    def __init__(self, workload: str, uniform: bool = False):
         import torch
 
         from paper_1610_05838_amd import datagen, mfsgd
@@ -86,7 +92,9 @@ class Runner:
         self.torch, self.datagen, self.M = torch, datagen, mfsgd
         self.dev = torch.device("cuda:0")
         torch.cuda.set_device(self.dev)
-        w = datagen.workload(workload)
+        w = datagen.workload(workload, **(dict(zipf_u=0.0, zipf_v=0.0) if uniform else {}))
+        if uniform:
+            w["name"] += " (uniform indices)"
         t0 = time.perf_counter()
         if w["draw"] == "independent":
             self.dS = datagen.draw_to_device(w, 0, w["ntrain"], self.dev)
@@ -105,6 +113,15 @@ class Runner:
         wavefronts, grouped four to a workgroup (one-wavefront teams when
         workers == s)."""
         w, M = self.w, self.M
+        if scheme == "table":
+            W = workers or 128
+            grid = s or min(1024, 2 * W)
+            opts = dict(dtype=1 if w["dtype"] == "fp16" else 0, batch_f=256, depth=2, table_grid=grid,
+                        table_workers=W, debug=0)
+            for key, val in opts.items():
+                M.set_option(key, val)
+            M.init(w["m"], w["n"], w["k"], w["seed"])
+            return W
         s = s or w.get("grid_s", 32)
         team = 0
         actual = workers
@@ -131,7 +148,7 @@ class Runner:
 
 
 def curves(args):
-    r = Runner(args.workload)
+    r = Runner(args.workload, args.uniform)
     w = r.w
     lr_t, lam = lr_schedule(w, args.lr)
     rows = []
@@ -161,14 +178,14 @@ def curves(args):
 
 
 def workers(args):
-    r = Runner(args.workload)
+    r = Runner(args.workload, args.uniform)
     w = r.w
     lr_t, lam = lr_schedule(w, "config")
     counts = [int(x) for x in args.counts.split(",")]
     table = {}
     for scheme, s in parse_schemes(args.schemes):
-        s_eff = s or w.get("grid_s", 32)
         for W in counts:
+            s_eff = (s or min(1024, 2 * W)) if scheme == "table" else (s or w.get("grid_s", 32))
             actual = r.setup(scheme, s, workers=W, partition=args.partition)
             if actual != W:
                 log(f"{label(scheme, s_eff)}: {W} workers is not a team shape (runs {actual}); skipped")
@@ -178,7 +195,7 @@ def workers(args):
             if W == 0 and scheme == "hogwild":
                 W = resident
             r.epoch_ms(scheme, lr_t(0), lam)
-            if scheme != "hogwild":
+            if scheme not in ("hogwild", "table"):
                 # workgroups per team as laid out (capped by the co-resident
                 # workgroups of the team's XCD); four wavefronts each, one for
                 # one-wavefront teams
@@ -189,7 +206,7 @@ def workers(args):
                     W = actual
             ms = min(r.epoch_ms(scheme, lr_t(1 + i), lam) for i in range(args.epochs))
             ups = w["ntrain"] / (ms / 1e3)
-            table[(label(scheme, s_eff), W)] = ups
+            table[(label(scheme, s), W)] = ups
             print(json.dumps({"exp": "workers", "workload": w["name"], "scheme": label(scheme, s_eff), "workers": W,
                               "resident_waves": resident, "epoch_ms": round(ms, 3), "updates_per_s": ups}),
                   flush=True)
@@ -214,6 +231,7 @@ def main():
     ap.add_argument("--partition", type=int, default=0,
                     help="batch-Hogwild! form: 0 one address space, 1 XCD-partitioned, 2 automatic")
     ap.add_argument("--counts", default="32,64,128,256,512,1024,2048,4096,8192")
+    ap.add_argument("--uniform", action="store_true", help="users and items drawn uniformly (no Zipf skew)")
     args = ap.parse_args()
     if args.exp == "curves":
         args.epochs = args.epochs or 20

@@ -80,3 +80,29 @@ def test_partitioned_form_at_full_size(M, netflix):
     assert bool(torch.all(M.debug_visits(len(S)) == 1))
     tr = M.debug_trace(x * x).cpu().numpy().reshape(x, x)
     assert np.array_equal(tr, oracle.wavefront_sigma(w["seed"], 0, x))
+
+
+def test_global_table_at_full_size_replays_serially(M, netflix):
+    """The global scheduling table at its bench setting (a 256 x 256 grid, 128
+    workers): every sample used once, and the factors equal the oracle's
+    serial update of the blocks in the order the trace records (blocks held at
+    once share no row and no column), within max-abs 1e-4; the test RMSE
+    kernel agrees with the oracle's on the result."""
+    import torch
+    w, S, T, dS, dT = netflix
+    reset(M, table_grid=256, table_workers=128, debug=3)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "table")
+    assert bool(torch.all(M.debug_visits(len(S)) == 1))
+    B = M.get_option("table_blocks")
+    tr = M.debug_trace(3 * B).cpu().numpy().reshape(-1, 3)
+    order, start = oracle.block_order(S, w["m"], w["n"], 256)
+    assert B == int(np.count_nonzero(np.diff(start)))
+    seq = np.concatenate([order[start[b]:start[b + 1]] for b in tr[:, 0]])
+    del order
+    Po, Qo = oracle.init_factors(w["m"], w["n"], w["k"], w["seed"], np.float32)
+    oracle.epoch_serial(Po, Qo, S[seq], w["lr"], w["lam"], w["lam"])
+    P, Q = M.get_factors(w["m"], w["n"], w["k"])
+    P, Q = P.cpu().numpy(), Q.cpu().numpy()
+    assert float(np.abs(P - Po).max()) <= 1e-4 and float(np.abs(Q - Qo).max()) <= 1e-4
+    assert M.rmse(dT) == pytest.approx(oracle.rmse(Po, Qo, T), rel=1e-5)

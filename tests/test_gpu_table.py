@@ -8,8 +8,10 @@ through the C ABI, against the CPU oracle.
   (binary32) / 2e-2 (binary16).
 * Many workers: every sample is used once, every non-empty block is taken once,
   and blocks that share a row block or a column block are never held at the
-  same time (claim/release stamps of one event counter); the test RMSE after 5
-  epochs is within 1e-3 (binary32) / 5e-3 (binary16) of the serial oracle's.
+  same time (claim/release stamps of one event counter); the factors equal the
+  oracle's serial update of the blocks in the order the trace records (within
+  the same max-abs bounds); the test RMSE after 5 epochs is within 1e-3
+  (binary32) / 5e-3 (binary16) of the serial oracle's.
 """
 import numpy as np
 import pytest
@@ -192,3 +194,37 @@ def test_table_errors_and_timeout(M):
     M.sync()
     assert M.get_option("table_blocks") == 16
     assert np.all(M.debug_visits(len(S)).cpu().numpy() == 1)
+
+
+def replay_order(S, m, n, s, trace_blocks):
+    """Sample positions in the order a table epoch used them: blocks in the
+    order they were taken, each block's samples in array order."""
+    order, start = oracle.block_order(S, m, n, s)
+    return np.concatenate([order[start[b]:start[b + 1]] for b in trace_blocks])
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("m,n,s,W", [(4000, 2000, 64, 32), (200_000, 20_000, 64, 48)])
+def test_table_concurrent_epoch_replays_serially(M, gen, dtype, m, n, s, W):
+    """Blocks held at the same time share no row and no column, so a
+    many-worker epoch equals the serial update of the blocks in the order they
+    were taken (recorded in the trace).  With rows handed between XCDs at
+    every block, this checks the release/acquire hand-over exactly; the second
+    shape's P (102 MB at binary32) is far larger than one XCD's L2.  Binary32:
+    two epochs; binary16: one, the span its 2e-2 bound is stated for (rounding
+    every store to binary16, on both sides in different arithmetic, drifts
+    further on the rows of the hottest items over more epochs)."""
+    w = gen.workload("netflix", m=m, n=n, ntrain=2_000_000, ntest=0)
+    S = gen.draw(w, 0, w["ntrain"])
+    k, seed = 128, w["seed"]
+    setup(M, m, n, k, seed, dtype, table_grid=s, table_workers=W, debug=2)
+    dS = M.samples_to_device(S)
+    B = int(np.count_nonzero(np.diff(oracle.block_order(S, m, n, s)[1])))
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(2 if dtype == np.float32 else 1):
+        M.epoch(dS, 0.01, 0.05, 0.05, "table")
+        tr = M.debug_trace(3 * B).cpu().numpy().reshape(-1, 3)
+        oracle.epoch_serial(Po, Qo, S[replay_order(S, m, n, s, tr[:, 0])], 0.01, 0.05, 0.05)
+    P, Q = factors(M, m, n, k, dtype)
+    print(f"m={m} s={s} W={W} maxabs P {maxabs(P, Po):.3g} Q {maxabs(Q, Qo):.3g}")
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
