@@ -184,6 +184,12 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *   "stage_samples" samples per chunk of mfsgd_epoch_staged (default 2^25,
  *                  402 MB per buffer; three device buffers, and three
  *                  pinned host buffers for pageable arrays).
+ *   "wave_launch"  MFSGD_WAVEFRONT_DET only: 1 runs every wave as a kernel
+ *                  launch of its own (worker i of wave w updates block
+ *                  (i, sigma_i(w)) serially; the launch boundary orders the
+ *                  waves, no tickets), a cross-check of the ticketed kernel
+ *                  whose factors it reproduces bit for bit; 0 (default) the
+ *                  persistent ticketed kernel.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and

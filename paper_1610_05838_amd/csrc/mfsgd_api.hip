@@ -32,6 +32,7 @@ struct Options {
     int64_t spin_limit = int64_t(1) << 24;
     int64_t skip_stores = 2;
     int64_t stage_samples = int64_t(1) << 25;
+    int64_t wave_launch = 0;
     int64_t table_grid = 256;
     int64_t table_workers = 0;
     int64_t debug = 0;
@@ -370,6 +371,7 @@ const OptSpec kOpts[] = {
     {"spin_limit", &Options::spin_limit, 1, 0xffffffffll, "spin_limit must be in [1, 2^32-1]"},
     {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
     {"stage_samples", &Options::stage_samples, 64, int64_t(1) << 31, "stage_samples must be in [64, 2^31]"},
+    {"wave_launch", &Options::wave_launch, 0, 1, "wave_launch must be 0 or 1"},
     {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
     {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
@@ -1099,11 +1101,23 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)s * s, st));
             a.trace_wave = c.trace;
         }
-        HIPCHK(reset_tickets(c.tickets, c.sched, st));
-        if (c.dtype == MFSGD_FP16)
-            HIPCHK(epoch_f16(a, st));
-        else
-            HIPCHK(epoch_f32(a, st));
+        if (scheme == MFSGD_WAVEFRONT_DET && g_opt.wave_launch) {
+            // the cross-check form: one launch per wave, ordered by the stream
+            a.scheme = kSchemeWaveLaunch;
+            for (int w = 0; w < s; ++w) {
+                a.wave = w;
+                if (c.dtype == MFSGD_FP16)
+                    HIPCHK(epoch_f16(a, st));
+                else
+                    HIPCHK(epoch_f32(a, st));
+            }
+        } else {
+            HIPCHK(reset_tickets(c.tickets, c.sched, st));
+            if (c.dtype == MFSGD_FP16)
+                HIPCHK(epoch_f16(a, st));
+            else
+                HIPCHK(epoch_f32(a, st));
+        }
     }
     c.epoch += 1;
     return MFSGD_OK;

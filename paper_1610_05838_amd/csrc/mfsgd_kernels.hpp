@@ -341,6 +341,38 @@ __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, con
     }
 }
 
+// One wave of the deterministic wavefront-update schedule per launch: the
+// cross-check of the ticketed kernel above.  Workgroup i (one wavefront) is
+// worker i and updates block (i, sigma_i(w)) serially in array order; the
+// blocks of one wave share no row and no column, and the launch boundary
+// orders consecutive waves (every write of wave w is visible to wave w + 1
+// on any XCD), so no ticket is needed.  Same update code, same per-block
+// order, hence the same factors bit for bit.
+template <int KP, typename T, int D, bool DBG>
+__global__ __launch_bounds__(64) void k_wave(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
+                                             int s, int w, uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
+                                             T* __restrict__ Q, float lr, float lp, float lq, int f, DebugSink dbg,
+                                             int32_t* trace)
+{
+    __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
+    if (threadIdx.x == 0) {
+        shuffle_perm(sigma_c, s, Cperm);
+        shuffle_perm(sigma_o, s, Ooff);
+    }
+    __syncthreads();
+    const int i = (int)blockIdx.x;
+    const int col = Cperm[(i + Ooff[w]) % s];
+    const int64_t b = (int64_t)i * s + col;
+    const int64_t lo = bstart[b], hi = bstart[b + 1];
+    if (trace && threadIdx.x == 0)
+        trace[(int64_t)i * s + w] = col;
+    DebugSink blk = dbg;
+    blk.trace = nullptr;
+    if (blk.orig)
+        blk.orig += lo;
+    run_worker<KP, T, D, DBG, false>(Sp + lo, hi - lo, 1, 0, f, P, Q, lr, lp, lq, blk);
+}
+
 template <int KP, typename T, int D>
 static int occupancy_blocked_t(int threads)
 {
@@ -450,6 +482,10 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         }
         hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st, a.S,
                            a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
+    } else if (a.scheme == kSchemeWaveLaunch) {
+        const DebugSink dbg{a.visits, a.orig, nullptr};
+        hipLaunchKernelGGL((k_wave<KP, T, D, DBG>), dim3((unsigned)a.s), dim3(64), 0, st, a.S, a.bstart, a.s, a.wave,
+                           a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, dbg, a.trace_wave);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
         // skipped stores only in epochs without debug output (they never change results)

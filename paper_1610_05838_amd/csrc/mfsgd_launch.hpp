@@ -13,13 +13,14 @@ constexpr int kMaxGrid = 64;      // largest wavefront-update grid side s
 constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never changes
 constexpr int kSchemeHogwild = 0;
 constexpr int kSchemeWavefront = 1;
+constexpr int kSchemeWaveLaunch = 2; // one deterministic wavefront-update wave per launch (cross-check)
 // block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team
 constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid;
 
 struct DebugSink;
 
 struct EpochLaunch {
-    int scheme;  // kSchemeHogwild or kSchemeWavefront
+    int scheme;  // kSchemeHogwild, kSchemeWavefront or kSchemeWaveLaunch
     int KP;      // padded row width
     int depth;   // samples in flight per wavefront
     const Sample* S;
@@ -44,6 +45,7 @@ struct EpochLaunch {
     int wg_waves;    // wavefronts per workgroup
     void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
     uint64_t sigma_c, sigma_o;
+    int wave;        // kSchemeWaveLaunch: the wave this launch runs
     uint32_t* tickets;
     uint32_t* sched; // claim state, kSchedWords entries (see k_blocked)
     uint32_t spin_limit;

@@ -21,7 +21,8 @@ pytestmark = pytest.mark.gpu
 
 TOL = {np.float32: 1e-4, np.float16: 2e-2}
 DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=2, team_waves=0, partition=2, hogwild_grid=0, balance=1,
-                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0)
+                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0,
+                wave_launch=0, table_grid=256, table_workers=0)
 
 
 @pytest.fixture(scope="module")
@@ -577,3 +578,41 @@ def test_ticket_timeout_is_reported(M):
     M.set_option("spin_limit", 1 << 24)
     M.epoch(dS, 0.001, 0.0, 0.0, "wavefront_det")
     M.sync()
+
+
+# ---------------------------------------------------------------------------- per-wave launches
+def _det_epochs(M, dS, w, s, epochs, **opts):
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    setup(M, m, n, k, seed, np.float16 if opts.pop("fp16", False) else np.float32, debug=2, **opts)
+    M.plan(dS, s)
+    traces = []
+    for t in range(epochs):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
+        traces.append(M.debug_trace(s * s).cpu().numpy())
+    P, Q = M.get_factors(m, n, k)
+    return P.cpu(), Q.cpu(), traces
+
+
+@pytest.mark.parametrize("fp16", [False, True])
+@pytest.mark.parametrize("s", [3, 8, 32])
+def test_wave_launches_equal_ticketed_kernel(M, gen, s, fp16):
+    """The deterministic schedule run as one kernel launch per wave (no
+    tickets; the launch boundary orders the waves) and as the persistent
+    ticketed kernel: same column orders, factors equal bit for bit, on the
+    tiny set and on Zipf-skewed k = 128 data (hot rows, skipped stores in the
+    ticketed kernel)."""
+    import torch
+    w = gen.workload("tiny")
+    S, _ = gen.make(w)
+    wz = gen.workload("netflix", m=20_000, n=3_000, ntrain=300_000, ntest=0)
+    Sz = gen.draw(wz, 0, wz["ntrain"])
+    for ww, SS in ((w, S), (wz, Sz)):
+        dS = M.samples_to_device(SS)
+        P1, Q1, t1 = _det_epochs(M, dS, ww, s, 2, fp16=fp16, wave_launch=0)
+        P2, Q2, t2 = _det_epochs(M, dS, ww, s, 2, fp16=fp16, wave_launch=1)
+        for a, b in zip(t1, t2):
+            assert np.array_equal(a, b)
+        assert torch.equal(P1, P2) and torch.equal(Q1, Q2)
+        for t, tr in enumerate(t2):
+            assert np.array_equal(tr.reshape(s, s), oracle.wavefront_sigma(ww["seed"], t, s))
+    M.set_option("wave_launch", 0)
