@@ -304,8 +304,15 @@ int64_t mfsgd_get_epoch(void);
  *                      started (wavefront epochs count by position in the
  *                      caller's array).
  *   MFSGD_DBG_TRACE  : batch-Hogwild!: dst int32[ceil(nnz/f)], the worker
- *                      that ran each batch; wavefront: dst int32[s*s],
- *                      entry i*s+w = column block of worker i in wave w;
+ *                      that ran each batch; wavefront and partitioned
+ *                      batch-Hogwild!: dst int32[s*s], entry i*s+w = column
+ *                      block of worker i in wave w, optionally followed by
+ *                      2*s*s values of one event counter (count up to
+ *                      3*s*s): entry s*s + 2(i*s+w) = the earliest claim of
+ *                      a batch of that block, the next entry = the completion
+ *                      of its last batch (the block of wave w+1 in the same
+ *                      column is claimed only after that; 0xffffffff where
+ *                      not recorded, e.g. per-wave launches);
  *                      global table: dst int32[3*B], B = "table_blocks": for
  *                      decision d, entry 3d = the block id I*s+J taken, 3d+1
  *                      and 3d+2 = the values of one event counter when the

@@ -1096,9 +1096,11 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.free_run = hog && g_opt.partition == 3 ? 1 : 0;
         a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
-            CHK(grow(&c.trace, &c.trace_cap, (int64_t)s * s, "trace"));
-            c.trace_n = (int64_t)s * s;
-            HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)s * s, st));
+            // columns, then two event stamps per (team, wave)
+            const int64_t words = 3 * (int64_t)s * s;
+            CHK(grow(&c.trace, &c.trace_cap, words, "trace"));
+            c.trace_n = words;
+            HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)words, st));
             a.trace_wave = c.trace;
         }
         if (scheme == MFSGD_WAVEFRONT_DET && g_opt.wave_launch) {

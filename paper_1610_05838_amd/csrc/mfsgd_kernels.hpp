@@ -67,8 +67,15 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
 // wavefront that then finds nothing to claim leaves, so the grid drains.
 //
 // sched: [0, G2) batches finished per (team, wave), [G2, 2 G2) next batch to
-// claim per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, where
-// G2 = kMaxGrid^2; all zero at launch.
+// claim per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, then one
+// event counter, where G2 = kMaxGrid^2; all zero at launch.
+//
+// Debug (trace != nullptr): trace[t*s + w] = column of team t in wave w, and
+// after those s*s entries two stamps per (team, wave) from the event counter:
+// the earliest claim of any of the block's batches and the completion of its
+// last batch (taken before the column's ticket moves on).  In every column,
+// the block of wave w+1 must be claimed only after the block of wave w was
+// completed; the host checks that from the stamps.
 template <int KP, typename T, int D, bool DBG, bool SKIP>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, const int32_t* __restrict__ tmap,
@@ -89,6 +96,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     uint32_t* const fin = sched;
     uint32_t* const claim = sched + kMaxGrid * kMaxGrid;
     uint32_t* const cursor = sched + 2 * kMaxGrid * kMaxGrid;
+    uint32_t* const events = cursor + kMaxGrid;
+    uint32_t* const stamps = trace ? reinterpret_cast<uint32_t*>(trace) + (int64_t)s * s : nullptr;
     // two private rows per wavefront of the grid for skipped stores
     T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
     if (threadIdx.x == 0) {
@@ -152,8 +161,14 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             // an empty block is released by its only claimant
             if (lane == 0) {
                 if (nb == 0 && idx == 0) {
-                    if (trace)
+                    if (trace) {
                         trace[tw] = col;
+                        const uint32_t e =
+                            __hip_atomic_fetch_add(events, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        stamps[2 * tw] = e;
+                        stamps[2 * tw + 1] = e + 1u;
+                        __builtin_amdgcn_s_waitcnt(0);
+                    }
                     __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
                 }
                 uint32_t expect = (uint32_t)w;
@@ -162,8 +177,13 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             }
             continue;
         }
-        if (trace && idx == 0 && lane == 0)
-            trace[tw] = col;
+        if (trace && lane == 0) {
+            if (idx == 0)
+                trace[tw] = col;
+            const uint32_t e = __hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_min(stamps + 2 * tw, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0); // stamped before any of the batch's rows is read
+        }
         if (entered != tw) {
             // the ticket was read before: rows of this block written on other
             // XCDs become visible once this wavefront's caches are invalidated
@@ -189,8 +209,14 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             // last batch of the block: every batch's stores are in this XCD's
             // L2; write it back, then pass the column on
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-            if (lane == 0)
+            if (lane == 0) {
+                if (trace) {
+                    stamps[2 * tw + 1] =
+                        __hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __builtin_amdgcn_s_waitcnt(0);
+                }
                 __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
     }
 }

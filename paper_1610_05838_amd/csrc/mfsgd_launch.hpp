@@ -14,8 +14,8 @@ constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never ch
 constexpr int kSchemeHogwild = 0;
 constexpr int kSchemeWavefront = 1;
 constexpr int kSchemeWaveLaunch = 2; // one deterministic wavefront-update wave per launch (cross-check)
-// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team
-constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid;
+// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team, event counter
+constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1;
 
 struct DebugSink;
 

@@ -616,3 +616,46 @@ def test_wave_launches_equal_ticketed_kernel(M, gen, s, fp16):
         for t, tr in enumerate(t2):
             assert np.array_equal(tr.reshape(s, s), oracle.wavefront_sigma(ww["seed"], t, s))
     M.set_option("wave_launch", 0)
+
+
+# ---------------------------------------------------------------------------- column hand-over (race check)
+def assert_column_handover(tr, s):
+    """From the trace of a ticketed block-scheduled epoch: every block was
+    claimed before it completed, and in every column the block of wave w+1 was
+    first claimed only after the block of wave w had completed."""
+    cols = tr[:s * s].reshape(s, s)
+    st = tr[s * s:3 * s * s].view(np.uint32).reshape(s, s, 2).astype(np.int64)
+    assert np.all(st != 0xFFFFFFFF), "a block has no stamps"
+    assert np.all(st[:, :, 0] < st[:, :, 1])
+    for w in range(s):
+        assert sorted(cols[:, w]) == list(range(s))
+    team_of = np.empty((s, s), dtype=np.int64)  # [column, wave] -> team
+    for t in range(s):
+        team_of[cols[t], np.arange(s)] = t
+    w = np.arange(s - 1)
+    for c in range(s):
+        prev, nxt = team_of[c, :-1], team_of[c, 1:]
+        assert np.all(st[nxt, w + 1, 0] > st[prev, w, 1]), f"column {c} was entered before it was handed over"
+    return int((st[:, :, 1] - st[:, :, 0]).max())
+
+
+@pytest.mark.parametrize("scheme,s,opts", [
+    ("wavefront", 32, {}), ("wavefront", 32, {"skip_stores": 1}), ("wavefront", 64, {"balance": 0}),
+    ("wavefront_det", 16, {}), ("hogwild", 8, {"partition": 1}), ("hogwild", 16, {"partition": 1, "hogwild_grid": 16}),
+])
+def test_column_handover_is_ordered(M, gen, scheme, s, opts):
+    """Race check of the ticket protocol under real concurrency (pooled teams,
+    Zipf-skewed blocks, rows handed between XCDs): claim and completion stamps
+    of one event counter order every column's blocks wave by wave."""
+    w = gen.workload("netflix", m=30_000, n=4_000, ntrain=800_000, ntest=0)
+    S = gen.draw(w, 0, w["ntrain"])
+    setup(M, w["m"], w["n"], 64, w["seed"], debug=3, **opts)
+    dS = M.samples_to_device(S)
+    if scheme != "hogwild":
+        M.plan(dS, s)
+    for t in range(2):
+        M.epoch(dS, 0.002, 0.01, 0.01, scheme)
+        assert bool((M.debug_visits(len(S)) == 1).all().item())
+        tr = M.debug_trace(3 * s * s).cpu().numpy()
+        assert np.array_equal(tr[:s * s].reshape(s, s), oracle.wavefront_sigma(w["seed"], t, s))
+        assert_column_handover(tr, s)
