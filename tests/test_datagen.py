@@ -88,3 +88,19 @@ def test_hugewiki_planted_rank(gen):
     Ps, Qs = gen.planted(w)
     assert Ps.shape == (100_000, 16) and Qs.shape == (w["n"], 16)
     assert float(Ps.var()) == pytest.approx(1 / math.sqrt(16), rel=0.01)
+
+
+def test_yahoo_shaped_ratings(gen):
+    """r = clamp(round(100 Phi(p*.q* + N(0, 0.25))), 0, 100) / 20: integer
+    percentiles over 0..100 (divided by 20), symmetric about 50 since
+    p*.q* + noise has mean 0, and heavier at the ends than a uniform because
+    its variance (1.25) exceeds the standard normal's."""
+    w = gen.workload("yahoo", m=20_000, n=15_000, ntrain=400_000, ntest=0)
+    r = gen.draw(w, 0, w["ntrain"])["r"].astype(np.float64) * 20  # r is stored in binary32
+    assert np.allclose(r, np.round(r), atol=1e-4) and r.min() >= 0 and r.max() <= 100
+    r = np.round(r)
+    h = np.bincount(r.astype(np.int64), minlength=101)
+    assert h[0] > 0 and h[100] > 0
+    assert abs(r.mean() - 50) < 1.0
+    # P(percentile <= 10) = P(Z * sqrt(1.25) <= Phi^-1(0.105)) ~ 0.13 > 0.105 (uniform)
+    assert 0.12 < h[:11].sum() / len(r) < 0.145
