@@ -136,7 +136,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build runs the SGD hot path on a single MI355X "
+        print("bench.py measures one GPU only: the library runs the SGD hot path on a single MI355X "
               "(multi-GPU sharding is a design note, not implemented)", file=sys.stderr)
         sys.exit(2)
 

@@ -16,7 +16,8 @@ and writes profiles/<kernel>_<workload>[_<scheme>].md (the summary, with the
 commands) and profiles/traffic_<kernel>_<scheme>_<workload>.json (scaled HBM
 bytes per launch and the digest of the kernel sources they were taken on;
 bench.py reports them as roofline.traffic only while that digest matches).
-Raw rocprofv3 output stays under --out (default gpurun_out/prof_<tag>).
+Raw rocprofv3 output stays under --out (default profiles/raw/prof_<tag>, not
+committed); the summary names that directory $OUT.
 With --summarize-only the passes are not run again.
 """
 from __future__ import annotations
@@ -134,7 +135,7 @@ def main():
     ap.add_argument("bench_args", nargs=argparse.REMAINDER, help="after --: more bench.py options")
     a = ap.parse_args()
     extra = [x for x in a.bench_args if x != "--"]
-    out = os.path.abspath(a.out or os.path.join(ROOT, "gpurun_out", f"prof_{a.workload}_{a.scheme}"))
+    out = os.path.abspath(a.out or os.path.join(ROOT, "profiles", "raw", f"prof_{a.workload}_{a.scheme}"))
     py = sys.executable or "python3"
     base = [py, os.path.join(ROOT, "bench.py"), "--workload", a.workload, "--scheme", a.scheme,
             "--no-cpu-baseline"] + extra
@@ -206,7 +207,7 @@ def main():
          "Made by `python3 bench_profile.py --workload " + a.workload + " --scheme " + a.scheme +
          (" -- " + " ".join(extra) if extra else "") + "`, which runs these passes (from /tmp):", ""]
     for key in ("trace", "FETCH_SIZE", "WRITE_SIZE"):
-        L.append("    " + " ".join(x.replace(ROOT, "$REPO") for x in cmds[key]))
+        L.append("    " + " ".join(x.replace(out, "$OUT").replace(ROOT, "$REPO") for x in cmds[key]))
     L += ["", "## Kernel statistics (kernel trace)", "",
           "| kernel | calls | average ms | min ms | max ms | share |", "|---|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
