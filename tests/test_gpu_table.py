@@ -130,7 +130,10 @@ def test_table_concurrent_schedule_is_conflict_free(M, s, W):
     ev[tr[:, 2]] = -1
     held = np.cumsum(ev).max()
     print(f"s={s} W={W} blocks={B} most held at once={held}")
-    assert 1 < held <= min(W, s)
+    assert 1 <= held <= min(W, s)
+    if s <= 128:
+        # blocks of ~40 or more samples: the lock is not the bottleneck, so workers overlap
+        assert held > 1
 
 
 @pytest.mark.parametrize("dtype,tol", [(np.float32, 1e-3), (np.float16, 5e-3)])
