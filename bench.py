@@ -131,6 +131,9 @@ def main():
     ap.add_argument("--staged", action="store_true",
                     help="training samples stay in pinned host memory and stream through the GPU (mfsgd_epoch_staged, "
                          "batch-Hogwild!): value then includes the PCIe transfers and is not the resident rate")
+    ap.add_argument("--log-jsonl", default="", metavar="PATH",
+                    help="also write one JSON row per timed epoch (epoch, ms, updates/s, algorithmic GB/s, fraction "
+                         "of the HBM peak, test RMSE) to PATH")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -222,6 +225,15 @@ def main():
     epoch_ms = [a.elapsed_time(b) for a, b in events]
     log(f"timed {args.steps} steps in {wall:.3f}s; epoch kernel ms: " + ", ".join(f"{x:.2f}" for x in epoch_ms))
     log(f"test rmse after each epoch: " + ", ".join(f"{x:.4f}" for x in rmses))
+    if args.log_jsonl:
+        bpu = 4 * w["k"] * (2 if w["dtype"] == "fp16" else 4) + 12
+        with open(args.log_jsonl, "w") as f:
+            for i, ms in enumerate(epoch_ms):
+                ups = nnz / (ms / 1e3)
+                f.write(json.dumps({"workload": w["name"], "scheme": args.scheme, "dtype": w["dtype"],
+                                    "epoch": args.warmup + i + 1, "epoch_ms": ms, "updates_per_s": ups,
+                                    "algorithmic_gbs": ups * bpu / 1e9, "frac_of_peak": ups * bpu / 1e9 / HBM_PEAK_GBS,
+                                    "test_rmse": rmses[args.warmup + i]}) + "\n")
 
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
@@ -242,7 +254,7 @@ def main():
     value = nnz * args.steps / wall
     key = f"{kernel}_{args.scheme}_{w['name']}"
     variant = [x for x in sys.argv[1:] if x not in ("--no-cpu-baseline", "--copy-calibration")]
-    drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus"}
+    drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus", "--log-jsonl"}
     variant = [x for i, x in enumerate(variant) if x not in drop and (i == 0 or variant[i - 1] not in drop)]
     traffic = measured_traffic(key, variant)
     out = {
