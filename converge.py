@@ -154,7 +154,7 @@ def curves(args):
     rows = []
     for scheme, s in parse_schemes(args.schemes):
         r.setup(scheme, s, partition=args.partition)
-        s_eff = s or w.get("grid_s", 32)
+        s_eff = (s or 256) if scheme == "table" else (s or w.get("grid_s", 32))
         elapsed, hist, hit = 0.0, [], None
         for t in range(args.epochs):
             ms = r.epoch_ms(scheme, lr_t(t), lam)
