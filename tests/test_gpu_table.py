@@ -186,6 +186,10 @@ def test_table_errors_and_timeout(M):
     dS = M.samples_to_device(S)
     M.epoch(dS[:0], 0.01, 0.0, 0.0, "table")
     M.sync()
+    # 2^32 samples or more are refused before any sample is read
+    import ctypes
+    rc = M.lib().mfsgd_epoch(ctypes.c_void_p(dS.data_ptr()), 1 << 32, 0.01, 0.0, 0.0, M.GLOBAL_TABLE, None)
+    assert rc == M.EINVAL and b"2^32" in M.lib().mfsgd_last_error()
     M.epoch(dS, 0.001, 0.0, 0.0, "table")
     with pytest.raises(M.MfsgdError) as e:
         M.sync()
