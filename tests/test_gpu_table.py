@@ -100,6 +100,20 @@ def test_table_single_worker_k128_zipf(M, gen, dtype, depth):
     assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [50, 300])  # padded widths 64 and 512
+def test_table_single_worker_other_widths(M, dtype, k):
+    rng = np.random.default_rng(k)
+    m, n, seed, s = 2000, 500, 99 + k, 16
+    S = rand_samples(rng, m, n, 60_001)
+    setup(M, m, n, k, seed, dtype, table_grid=s, table_workers=1)
+    M.epoch(M.samples_to_device(S), 0.01, 0.03, 0.04, "table")
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    oracle.epoch_table(Po, Qo, S, 0.01, 0.03, 0.04, s, seed, 0)
+    P, Q = factors(M, m, n, k, dtype)
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+
+
 @pytest.mark.parametrize("s,W", [(128, 64), (64, 200), (512, 256)])
 def test_table_concurrent_schedule_is_conflict_free(M, s, W):
     """Many workers: each non-empty block taken once, each sample used once,
