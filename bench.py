@@ -283,6 +283,7 @@ def main():
                      "bytes_per_update": bytes_per_update, "updates_per_launch": nnz,
                      "avg_launch_ms": avg_epoch_s * 1e3},
         "epoch_updates_per_s": nnz / avg_epoch_s,
+        "median_epoch_ms": sorted(epoch_ms)[len(epoch_ms) // 2],
         "test_rmse": rmses[-1],
     }
     if args.scheme == "table":
