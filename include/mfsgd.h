@@ -73,7 +73,11 @@ enum {
      * never lock.  With option "partition" = 0 the whole array is
      * split into batches, batch b going to worker (wavefront) b mod W, over
      * the whole GPU in one address space: updates made on one XCD reach the
-     * others as lines are written back and evicted (see "sync_every").  With
+     * others as lines are written back and evicted (see "sync_every"); a row
+     * that several XCDs keep cached is updated in separate copies of which the
+     * one written back last wins, so on data with very popular rows the
+     * per-epoch convergence trails the serial order (batch-Hogwild! inside
+     * one XCD does not).  With
      * "partition" = 1 the rating matrix is cut into an s x s grid (s = number
      * of XCDs unless "hogwild_grid" says otherwise; planned internally, once
      * per sample array) and the wavefronts of each XCD run batch-Hogwild!
@@ -96,7 +100,8 @@ enum {
     MFSGD_WAVEFRONT = 1,
     /* the same schedule with one wavefront per worker and each block's
      * samples in their array order: the result then equals the serial
-     * update in wave order up to floating-point rounding (deterministic). */
+     * update in wave order up to floating-point rounding (deterministic).
+     * Option "wave_launch" runs it as one kernel launch per wave instead. */
     MFSGD_WAVEFRONT_DET = 2,
     /* LIBMF's global scheduling table (section 3.2.1), the baseline the two
      * schedules above replace ("LIBMF-GPU" in the paper).  R is cut into a
