@@ -244,10 +244,13 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
 // has taken a block invalidates its caches (agent-scope acquire) before it
 // reads the rows.
 //
-// Nothing waits for a particular wavefront, and no wavefront leaves while it
-// holds the lock or a block; a worker that finds the lock taken or no block
-// free polls (with a sleep), and after spin_limit polls in a row raises *err,
-// upon which every worker leaves at its next visit to the table.
+// The lock is a ticket lock: a worker draws a ticket once and then only reads
+// the serving counter until its turn; the holder passes the lock on to the
+// next ticket.  No wavefront leaves while it holds the lock or a block; a
+// worker that waits for its turn, or finds no block free, polls (with a
+// sleep), and after spin_limit polls in a row raises *err, upon which every
+// worker leaves at its next visit to the table (a worker whose ticket is
+// never served because its predecessor gave up leaves the same way).
 template <int KP, typename T, int D, bool DBG>
 __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                               int s, uint32_t nb, uint64_t draw, T* __restrict__ P,
@@ -255,27 +258,34 @@ __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, con
                                               uint32_t spin_limit, int* err, DebugSink dbg, int32_t* trace)
 {
     const int lane = lane_id();
-    uint32_t* const lock = tab;
+    uint32_t* const serving = tab;     // ticket now holding the table
     uint32_t* const left = tab + 1;
     uint32_t* const events = tab + 2;
+    uint32_t* const next_ticket = tab + 3;
     uint32_t* const row_used = tab + kTableHdr;
     uint32_t* const col_used = row_used + s;
     uint32_t* const list = col_used + s;
     const uint32_t us = (uint32_t)s;
     uint32_t polls = 0;
+    uint32_t ticket = 0;
+    bool queued = false;
     for (;;) {
-        // take the lock (test, then test-and-set)
+        // take the lock: a ticket lock (first come, first served), so waiting
+        // workers only read the serving counter instead of competing in
+        // atomic exchanges
         int got = 0, stop = 0;
         if (lane == 0) {
             stop = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
-            if (!stop && __hip_atomic_load(lock, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-                uint32_t expect = 0u;
-                got = __hip_atomic_compare_exchange_strong(lock, &expect, 1u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT);
+            if (!stop) {
+                if (!queued)
+                    ticket = __hip_atomic_fetch_add(next_ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                got = __hip_atomic_load(serving, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ticket;
             }
         }
         if (__builtin_amdgcn_readfirstlane(stop))
             return;
+        ticket = __builtin_amdgcn_readfirstlane(ticket);
+        queued = true;
         bool wait = !__builtin_amdgcn_readfirstlane(got);
         uint32_t fpos = 0, fblk = 0, d = 0;
         if (!wait) {
@@ -285,7 +295,7 @@ __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, con
             rem = __builtin_amdgcn_readfirstlane(rem);
             if (rem == 0u) {
                 if (lane == 0)
-                    __hip_atomic_store(lock, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(serving, ticket + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 return; // every block has been taken
             }
             d = nb - rem;
@@ -325,10 +335,11 @@ __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, con
                         trace[3 * (int64_t)d + 1] = (int32_t)stamp;
                     }
                 }
-                // every table write has completed before the lock is free
+                // every table write has completed before the lock passes on
                 __builtin_amdgcn_s_waitcnt(0);
-                __hip_atomic_store(lock, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(serving, ticket + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            queued = false; // the next attempt takes a new ticket
             wait = !found;
         }
         if (wait) {

@@ -58,8 +58,9 @@ struct EpochLaunch {
 };
 
 // Global scheduling table (LIBMF's policy, the baseline of section 3.2.1).
-// tab, in 32-bit words: [0] lock, [1] blocks not yet taken this epoch,
-// [2] event counter (debug stamps), [kTableHdr, +s) row block in use,
+// tab, in 32-bit words: [0] ticket now served (the lock), [1] blocks not yet
+// taken this epoch, [2] event counter (debug stamps), [3] next ticket,
+// [kTableHdr, +s) row block in use,
 // [kTableHdr + s, +s) column block in use, [kTableHdr + 2 s, + nb) the blocks
 // not yet taken.
 constexpr int kMaxTableGrid = 1024; // largest grid side of the table
