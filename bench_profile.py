@@ -208,7 +208,8 @@ def main():
          (" -- " + " ".join(extra) if extra else "") + "`, which runs these passes (from /tmp):", ""]
     for key in ("trace", "FETCH_SIZE", "WRITE_SIZE"):
         L.append("    " + " ".join(x.replace(out, "$OUT").replace(ROOT, "$REPO") for x in cmds[key]))
-    L += ["", "## Kernel statistics (kernel trace)", "",
+    L += ["", "$OUT is the directory the raw rocprofv3 output was written to (not committed).",
+          "", "## Kernel statistics (kernel trace)", "",
           "| kernel | calls | average ms | min ms | max ms | share |", "|---|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
         L.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.3f} | "
