@@ -108,6 +108,80 @@ def cpu_baseline(w, S, target_s: float, threads: int):
     return serial, omp
 
 
+XGMI_LINK_GBS = 153.0  # one MI355X xGMI link, per direction (published figure, not measured here)
+
+
+def shard_share(args):
+    """One GPU's share of a G-GPU epoch under the block partition of the
+    paper's section 4.1, measured on this GPU at its real shape.  R is cut
+    into G x G blocks by equal user and item ranges; GPU g keeps user segment
+    g of P for the whole epoch and in wave w updates block (g, (g + w) mod G)
+    while item segment (g + w) mod G of Q travels to it from its neighbour.
+    Here g = 0: the share's samples are generated, bucketed by item segment,
+    and each wave's block is one batch-Hogwild! epoch over that block's
+    samples (the kernel touches only the rows of its segments).  The wave's
+    Q-segment message is priced at one xGMI link's rate."""
+    import numpy as np
+    import torch
+
+    from paper_1610_05838_amd import datagen, mfsgd
+
+    G = args.shard
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = datagen.workload(args.workload)
+    if args.ntrain:
+        w["ntrain"] = args.ntrain
+    m, n, k, nnz = w["m"], w["n"], w["k"], w["ntrain"]
+    t0 = time.perf_counter()
+    blocks = [[] for _ in range(G)]
+    chunk = 1 << 25
+    for c0 in range(0, nnz, chunk):
+        S = datagen.draw(w, c0, min(chunk, nnz - c0)) if w["draw"] == "independent" else datagen.make(w)[0]
+        mine = S[(S["u"].astype(np.int64) * G) // m == 0]
+        seg = (mine["v"].astype(np.int64) * G) // n
+        for j in range(G):
+            blocks[j].append(mine[seg == j])
+        if w["draw"] != "independent":
+            break
+    blocks = [np.concatenate(b) for b in blocks]
+    share = sum(len(b) for b in blocks)
+    log(f"share of GPU 0 of {G}: {share} of {nnz} samples in {time.perf_counter() - t0:.1f}s")
+    dtype = 1 if w["dtype"] == "fp16" else 0
+    feat = 2 if dtype else 4
+    # one address space inside each block: its working set is one user and one item segment
+    for key, val in dict(dtype=dtype, batch_f=256, workers=args.workers, depth=args.depth, partition=0,
+                         debug=0).items():
+        mfsgd.set_option(key, val)
+    mfsgd.init(m, n, k, w["seed"])
+    stream = torch.cuda.current_stream()
+    dB = [mfsgd.samples_to_device(b, dev) for b in blocks]
+    wave_ms = np.zeros(G)
+    epochs = max(1, args.steps)
+    for t in range(args.warmup + epochs):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(G)]
+        for wv in range(G):  # GPU 0 works on item segment wv in wave wv
+            ev[wv][0].record(stream)
+            mfsgd.epoch(dB[wv], datagen.lr_at(w, t), w["lam"], w["lam"], "hogwild", stream)
+            ev[wv][1].record(stream)
+        torch.cuda.synchronize()
+        if t >= args.warmup:
+            wave_ms += np.array([a.elapsed_time(b) for a, b in ev]) / epochs
+    q_bytes = -(-n // G) * k * feat
+    xfer_ms = q_bytes / (XGMI_LINK_GBS * 1e9) * 1e3
+    proj_ms = float(np.maximum(wave_ms, xfer_ms).sum())
+    mfsgd.finalize()
+    print(json.dumps({
+        "mode": "shard", "workload": w["name"], "gpus_emulated": G, "rank": 0, "k": k, "dtype": w["dtype"],
+        "share_samples": share, "total_samples": nnz, "wave_samples": [len(b) for b in blocks],
+        "wave_ms": [round(x, 3) for x in wave_ms], "compute_ms_per_epoch": round(float(wave_ms.sum()), 3),
+        "share_updates_per_s": share / (wave_ms.sum() / 1e3),
+        "q_segment_bytes": q_bytes, "xgmi_link_gbs_assumed": XGMI_LINK_GBS, "transfer_ms_per_wave": round(xfer_ms, 4),
+        "projected_epoch_ms": round(proj_ms, 3),
+        "note": "rank 0's share only; under skewed data the ranks' shares differ, and the slowest sets the epoch"}),
+        flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +208,9 @@ def main():
     ap.add_argument("--log-jsonl", default="", metavar="PATH",
                     help="also write one JSON row per timed epoch (epoch, ms, updates/s, algorithmic GB/s, fraction "
                          "of the HBM peak, test RMSE) to PATH")
+    ap.add_argument("--shard", type=int, default=0, metavar="G",
+                    help="measure one GPU's share of a G-GPU run instead (the block partition of the paper's section "
+                         "4.1: GPU 0 keeps user segment 0 and takes item segment w in wave w); prints its own JSON line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -142,6 +219,10 @@ def main():
         print("bench.py measures one GPU only: the library runs the SGD hot path on a single MI355X "
               "(multi-GPU sharding is a design note, not implemented)", file=sys.stderr)
         sys.exit(2)
+
+    if args.shard > 1:
+        shard_share(args)
+        return
 
     import numpy as np
     import torch
