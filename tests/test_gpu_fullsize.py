@@ -107,3 +107,22 @@ def test_global_table_at_full_size_replays_serially(M, netflix):
     P, Q = P.cpu().numpy(), Q.cpu().numpy()
     assert float(np.abs(P - Po).max()) <= 1e-4 and float(np.abs(Q - Qo).max()) <= 1e-4
     assert M.rmse(dT) == pytest.approx(oracle.rmse(Po, Qo, T), rel=1e-5)
+
+
+def test_deterministic_wavefront_at_full_size_matches_oracle(M, netflix):
+    """Deterministic wavefront-update on the full Netflix shape (32 x 32 grid cut
+    by sample counts, one wavefront per worker): every factor entry within
+    max-abs 1e-4 of the oracle's serial-equivalent wave order after one epoch."""
+    w, S, T, dS, dT = netflix
+    s = 32
+    reset(M, balance=1)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    M.plan(dS, s)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront_det")
+    P, Q = M.get_factors(w["m"], w["n"], w["k"])
+    P, Q = P.cpu().numpy(), Q.cpu().numpy()
+    Po, Qo = oracle.init_factors(w["m"], w["n"], w["k"], w["seed"], np.float32)
+    oracle.epoch_wavefront(Po, Qo, S, w["lr"], w["lam"], w["lam"], s, w["seed"], 0, balanced=True)
+    print(f"full-size deterministic wavefront: max-abs P {np.abs(P - Po).max():.3g} Q {np.abs(Q - Qo).max():.3g}")
+    assert float(np.abs(P - Po).max()) <= 1e-4 and float(np.abs(Q - Qo).max()) <= 1e-4
+    assert M.rmse(dT) == pytest.approx(oracle.rmse(Po, Qo, T), rel=1e-5)
