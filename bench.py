@@ -197,6 +197,8 @@ def main():
     ap.add_argument("--team-waves", type=int, default=0)
     ap.add_argument("--partition", type=int, default=2, help="batch-Hogwild!: 0 one address space, 1 XCD-partitioned, 2 automatic")
     ap.add_argument("--ntrain", type=int, default=0, help="override the training size (0: the workload's)")
+    ap.add_argument("--k", type=int, default=0,
+                    help="train at this width instead of the workload's (same samples; 0: the workload's k)")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
                     help="further library option (mfsgd_set_option), applied before init")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -253,6 +255,8 @@ def main():
         dS = mfsgd.samples_to_device(S, dev)
     dT = mfsgd.samples_to_device(T, dev)
     nnz = w["ntrain"]
+    if args.k:
+        w["k"] = args.k  # after generation: only the trained width changes
     log(f"generated {w['name']}: {nnz} train + {len(T)} test in {time.perf_counter() - t0:.1f}s")
 
     dtype = 1 if w["dtype"] == "fp16" else 0
@@ -267,6 +271,8 @@ def main():
     resident = mfsgd.get_option("resident_waves")
     partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged
     kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
+    if kernel == "k_hogwild" and w["k"] <= 32 and mfsgd.get_option("half_waves"):
+        kernel = "k_hogwild_half"
     grid_s = args.grid_s or w.get("grid_s", 32)
     if args.scheme == "table":
         kernel = "k_table"
@@ -333,7 +339,7 @@ def main():
     avg_epoch_s = sum(epoch_ms) / len(epoch_ms) / 1e3
     achieved_gbs = nnz * bytes_per_update / avg_epoch_s / 1e9
     value = nnz * args.steps / wall
-    key = f"{kernel}_{args.scheme}_{w['name']}"
+    key = f"{kernel}_{args.scheme}_{w['name']}" + (f"_k{args.k}" if args.k else "")
     variant = [x for x in sys.argv[1:] if x not in ("--no-cpu-baseline", "--copy-calibration")]
     drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus", "--log-jsonl"}
     variant = [x for i, x in enumerate(variant) if x not in drop and (i == 0 or variant[i - 1] not in drop)]

@@ -164,9 +164,10 @@ def main():
     kernel = a.kernel
     if not kernel:
         tot = {k: sum(float(r["TotalDurationNs"]) for r in stats if short(r["Name"]).split("<")[0].endswith(k))
-               for k in ("k_hogwild", "k_blocked", "k_table")}
+               for k in ("k_hogwild", "k_hogwild_half", "k_blocked", "k_table")}
         kernel = max(tot, key=tot.get)
-    tag = f"{kernel}_{a.workload}" + ("" if a.scheme == "hogwild" else f"_{a.scheme}")
+    kw = int(extra[extra.index("--k") + 1]) if "--k" in extra else 0
+    tag = f"{kernel}_{a.workload}" + ("" if a.scheme == "hogwild" else f"_{a.scheme}") + (f"_k{kw}" if kw else "")
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in trace
             if short(r["Kernel_Name"]).split("<")[0].endswith(kernel)]
     if not durs:
@@ -195,7 +196,7 @@ def main():
     nnz = w["ntrain"] if w else None
     if w and "--ntrain" in extra:
         nnz = int(extra[extra.index("--ntrain") + 1])
-    k = w["k"] if w else 128
+    k = kw or (w["k"] if w else 128)
     fb = 2 if (w and w["dtype"] == "fp16") else 4
     bpu = 4 * k * fb + 12
     hbm = per_launch["FETCH_SIZE"][1] + per_launch["WRITE_SIZE"][1]
@@ -233,7 +234,7 @@ def main():
               f"{hbm / avg_ns:.1f} GB/s ({100 * hbm / avg_ns / bench.HBM_PEAK_GBS:.1f}% of 8 TB/s)."]
     with open(md, "w") as f:
         f.write("\n".join(L) + "\n")
-    tj = os.path.join(bench.PROFILE_DIR, f"traffic_{kernel}_{a.scheme}_{a.workload}.json")
+    tj = os.path.join(bench.PROFILE_DIR, f"traffic_{kernel}_{a.scheme}_{a.workload}" + (f"_k{kw}" if kw else "") + ".json")
     with open(tj, "w") as f:
         json.dump({"kernel": kernel, "workload": a.workload, "scheme": a.scheme,
                    "bench_args": extra, "source_digest": bench.source_digest(),

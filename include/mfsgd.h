@@ -71,8 +71,9 @@ enum {
     /* batch-Hogwild! (section 3.2.2): samples are taken in batches of f
      * consecutive samples, each batch updated serially by one worker, workers
      * never lock.  With option "partition" = 0 the whole array is
-     * split into batches, batch b going to worker (wavefront) b mod W, over
-     * the whole GPU in one address space: updates made on one XCD reach the
+     * split into batches, batch b going to worker (wavefront; half-wavefront
+     * at k <= 32, see "half_waves") b mod W, over the whole GPU in one
+     * address space: updates made on one XCD reach the
      * others as lines are written back and evicted (see "sync_every"); a row
      * that several XCDs keep cached is updated in separate copies of which the
      * one written back last wins, so on data with very popular rows the
@@ -195,6 +196,13 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  waves, no tickets), a cross-check of the ticketed kernel
  *                  whose factors it reproduces bit for bit; 0 (default) the
  *                  persistent ticketed kernel.
+ *   "half_waves"   one-address-space batch-Hogwild! with k <= 32: 1
+ *                  (default) runs two workers per wavefront, one per half
+ *                  of its 64 lanes (a row of 32 values fills a half), so
+ *                  "workers" and the default worker count are then counted
+ *                  in half-wavefronts; 0 one worker per wavefront, whose
+ *                  upper 32 lanes idle.  A lone worker computes the same
+ *                  bits either way.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and

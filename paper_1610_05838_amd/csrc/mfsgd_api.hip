@@ -33,6 +33,7 @@ struct Options {
     int64_t skip_stores = 2;
     int64_t stage_samples = int64_t(1) << 25;
     int64_t wave_launch = 0;
+    int64_t half_waves = 1;
     int64_t table_grid = 256;
     int64_t table_workers = 0;
     int64_t debug = 0;
@@ -287,9 +288,13 @@ int padded_width(int k)
     return 512;
 }
 
+// Whether one-address-space batch-Hogwild! runs two workers per wavefront.
+bool half_wave_workers(int KP) { return KP == 32 && g_opt.half_waves != 0; }
+
 int occupancy_waves(int KP, int dtype, int depth)
 {
-    return dtype == MFSGD_FP16 ? occupancy_f16(KP, depth) : occupancy_f32(KP, depth);
+    const int half = half_wave_workers(KP) ? 1 : 0;
+    return dtype == MFSGD_FP16 ? occupancy_f16(KP, depth, half) : occupancy_f32(KP, depth, half);
 }
 
 int occupancy_blocked(int KP, int dtype, int depth, int threads)
@@ -372,6 +377,7 @@ const OptSpec kOpts[] = {
     {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
     {"stage_samples", &Options::stage_samples, 64, int64_t(1) << 31, "stage_samples must be in [64, 2^31]"},
     {"wave_launch", &Options::wave_launch, 0, 1, "wave_launch must be 0 or 1"},
+    {"half_waves", &Options::half_waves, 0, 1, "half_waves must be 0 or 1"},
     {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
     {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
@@ -1054,10 +1060,11 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);
             if (per_cu <= 0)
                 return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
-            W = (int64_t)c.cus * per_cu;
+            W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP) ? 2 : 1);
         }
         W = std::min(W, nbatch);
         a.scheme = kSchemeHogwild;
+        a.half = half_wave_workers(c.KP) ? 1 : 0;
         a.S = (const Sample*)samples;
         a.W = W;
         a.sync_every = (int)g_opt.sync_every;
@@ -1219,8 +1226,9 @@ int epoch_staged_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float 
         const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);
         if (per_cu <= 0)
             return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
-        W = (int64_t)c.cus * per_cu;
+        W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP) ? 2 : 1);
     }
+    a.half = half_wave_workers(c.KP) ? 1 : 0;
     if (dbg & 1) {
         CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
         c.visits_n = nnz;

@@ -134,7 +134,10 @@ __device__ __forceinline__ float dpp_mov(float x)
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 
-__device__ __forceinline__ float wave_sum(float x)
+// Sum over each half of the wavefront on its own: lanes 0-31 receive the sum
+// of lanes 0-31, lanes 32-63 that of lanes 32-63 (the first steps of
+// wave_sum, which therefore adds the same terms in the same order).
+__device__ __forceinline__ float half_sum(float x)
 {
     x += dpp_mov<0xB1>(x);  // quad_perm [1,0,3,2]: pairs
     x += dpp_mov<0x4E>(x);  // quad_perm [2,3,0,1]: quads
@@ -147,6 +150,12 @@ __device__ __forceinline__ float wave_sum(float x)
         auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
         x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
     }
+    return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x)
+{
+    x = half_sum(x);
     {
         auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
         x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
@@ -546,6 +555,225 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         if (!chunk(cU, cV, cR, ccnt, nU, nV, nR, ncnt))
             return;
         if (!chunk(nU, nV, nR, ncnt, cU, cV, cR, ccnt))
+            return;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Two batch-Hogwild! workers per wavefront, for rows of 32 values (KP = 32),
+// where a one-worker wavefront would leave half of its lanes idle.
+//
+// Lanes 0-31 are worker 2 h and lanes 32-63 worker 2 h + 1 of the W workers
+// (h = the wavefront's index); each half holds one value of a row per lane and
+// runs the sequence of run_worker's worker (batches b = worker, worker+W, ...
+// of f consecutive samples, in array order) with the same in-flight window,
+// forwarding and arithmetic.  The two halves step through their sequences
+// together: batch b of lanes 0-31 goes with batch b + 1 of lanes 32-63 at the
+// same offset, so the chunk offset is common and only the sample counts
+// differ (the second half's count never exceeds the first's, its samples lying
+// f further on).  A position past a half's count loads row 0 and stores
+// nothing.  Each half's dot product is a 32-lane sum; with one active half it
+// adds the same terms in the same order as run_worker's 64-lane sum (whose
+// idle lanes add zeros), so a lone worker computes the same bits either way.
+// ---------------------------------------------------------------------------
+template <typename T, int D, bool DBG, bool BUF = false>
+__device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t wave,
+                                                int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
+                                                float lq, const DebugSink dbg,
+                                                const CacheSync sync = CacheSync{0, false, false})
+{
+    constexpr int KP = 32;
+    constexpr int H = 32; // positions per chunk and half
+    static_assert(!BUF || sizeof(T) == 4, "buffer rows: one dword per lane");
+    static_assert(H % D == 0 && D <= 16, "depth must divide 32");
+
+    const int lane = lane_id();
+    const bool hi = lane >= H;           // lanes 32-63
+    const int col = lane & (H - 1);       // value of a row held by this lane
+    const int64_t w0 = 2 * wave;          // worker of lanes 0-31
+    const bool two = w0 + 1 < W;          // lanes 32-63 are a worker too
+    const Buf bp(P), bq(Q);
+    const uint32_t cb = (uint32_t)(col * sizeof(T));
+    constexpr uint32_t kRowBytes = (uint32_t)(KP * sizeof(T));
+    const float decay_p = lr * lp, decay_q = lr * lq;
+
+    // batch of lanes 0-31 (lanes 32-63 work on the next one) and common offset
+    int64_t c_batch = w0, n_batch = w0;
+    int c_off = 0, n_off = 0;
+    auto advance = [&](int64_t& b, int& o) {
+        o += H;
+        if (o >= f) {
+            o = 0;
+            b += W;
+        }
+    };
+    auto count = [&](int64_t s0) -> int {
+        const int64_t rem = nnz - s0;
+        return rem <= 0 ? 0 : (rem >= H ? H : (int)rem);
+    };
+    // metadata of one chunk: lane i of each half holds that half's sample i
+    auto load_chunk = [&](int64_t b, int o, int& cu, int& cv, float& cr, int& c0, int& c1) {
+        const int64_t s0 = b * (int64_t)f + o;
+        c0 = count(s0);
+        c1 = two ? count(s0 + f) : 0;
+        const int mine = hi ? c1 : c0;
+        const int64_t i = s0 + (hi ? f : 0) + (col < mine ? col : 0);
+        const Sample* sp = S + (mine > 0 ? i : 0);
+        cu = __builtin_nontemporal_load(&sp->u);
+        cv = __builtin_nontemporal_load(&sp->v);
+        cr = __builtin_nontemporal_load(&sp->r);
+    };
+
+    if (nnz <= 0 || w0 >= W || w0 * (int64_t)f >= nnz)
+        return;
+    int cU, cV, nU, nV, c0, c1, n0, n1;
+    float cR, nR;
+    load_chunk(c_batch, c_off, cU, cV, cR, c0, c1);
+    advance(n_batch, n_off);
+    load_chunk(n_batch, n_off, nU, nV, nR, n0, n1);
+
+    int su[D], sv[D], hu[D], hv[D];
+    float sr[D];
+    T sp[D], sq[D], hp[D], hq[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        su[d] = sv[d] = hu[d] = hv[d] = -1;
+        sr[d] = 0.f;
+        sp[d] = sq[d] = hp[d] = hq[d] = T{};
+    }
+
+    // request the rows of each half's sample at position xl of a chunk
+    auto issue = [&](int slot, int mu, int mv, float mr, int xl, int k0, int k1) {
+        const bool ok = xl < (hi ? k1 : k0);
+        const int u0 = __builtin_amdgcn_readlane(mu, xl), u1 = __builtin_amdgcn_readlane(mu, xl + H);
+        const int v0 = __builtin_amdgcn_readlane(mv, xl), v1 = __builtin_amdgcn_readlane(mv, xl + H);
+        const int r0 = __builtin_amdgcn_readlane(__float_as_int(mr), xl);
+        const int r1 = __builtin_amdgcn_readlane(__float_as_int(mr), xl + H);
+        const int u = hi ? u1 : u0, v = hi ? v1 : v0;
+        su[slot] = ok ? u : -1;
+        sv[slot] = ok ? v : -1;
+        sr[slot] = __int_as_float(hi ? r1 : r0);
+        if constexpr (BUF) {
+            sp[slot] = bp.template ld<T>(cb + (uint32_t)(ok ? u : 0) * kRowBytes, 0);
+            sq[slot] = bq.template ld<T>(cb + (uint32_t)(ok ? v : 0) * kRowBytes, 0);
+        } else {
+            sp[slot] = P[(int64_t)(ok ? u : 0) * KP + col];
+            sq[slot] = Q[(int64_t)(ok ? v : 0) * KP + col];
+        }
+    };
+
+    // update each half's sample in slot j (pos: position of the first half's
+    // sample in S; the second half's is f further)
+    auto process = [&](int j, int64_t pos) {
+        const int u = su[j], v = sv[j];
+        T pv = sp[j], qv = sq[j];
+        bool fwd = false;
+#pragma unroll
+        for (int d = 1; d < D; ++d) {
+            const int h = (j - d + D) % D;
+            fwd |= (hu[h] == u) | (hv[h] == v);
+        }
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(fwd) != 0, 0)) {
+#pragma unroll
+            for (int d = D - 1; d >= 1; --d) {
+                const int h = (j - d + D) % D;
+                pv = pick(hu[h] == u, hp[h], pv);
+                qv = pick(hv[h] == v, hq[h], qv);
+            }
+        }
+        const float pe = (float)pv, qe = (float)qv;
+        // the product is rounded before the sum (the empty asm keeps it from
+        // fusing into the first cross-lane add), as in run_worker
+        float dot = pe * qe;
+        asm volatile("" : "+v"(dot));
+        const float err = sr[j] - half_sum(dot);
+        float p[1], q[1];
+        if constexpr (sizeof(T) == 2) {
+            const float step = lr * err;
+            p[0] = __builtin_fmaf(-decay_p, pe, __builtin_fmaf(step, qe, pe));
+            q[0] = __builtin_fmaf(-decay_q, qe, __builtin_fmaf(step, pe, qe));
+        } else {
+            p[0] = pe + lr * (err * qe - lp * pe);
+            q[0] = qe + lr * (err * pe - lq * qe);
+        }
+        const T np = Row<T, 1>::narrow(p), nq = Row<T, 1>::narrow(q);
+        if (u >= 0) {
+            if constexpr (BUF) {
+                bp.template st<T>(np, cb + (uint32_t)u * kRowBytes, 0);
+                bq.template st<T>(nq, cb + (uint32_t)v * kRowBytes, 0);
+            } else {
+                P[(int64_t)u * KP + col] = np;
+                Q[(int64_t)v * KP + col] = nq;
+            }
+        }
+        hu[j] = u;
+        hv[j] = v;
+        hp[j] = np;
+        hq[j] = nq;
+        if constexpr (DBG) {
+            if (dbg.visits && col == 0 && u >= 0) {
+                const int64_t at = pos + (hi ? f : 0);
+                atomicAdd(dbg.visits + (dbg.orig ? dbg.orig[at] : at), 1u);
+            }
+        }
+    };
+
+    int batches = 0;
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d)
+        issue(d, cU, cV, cR, d, c0, c1);
+
+    // one chunk of H positions per half: metadata of this chunk in (aU, aV,
+    // aR; counts a0, a1), of the next in (bU, bV, bR; b0, b1); the registers of
+    // a finished chunk receive the chunk after next
+    auto chunk = [&](int& aU, int& aV, float& aR, int& a0, int& a1, int bU, int bV, float bR, int b0,
+                     int b1) -> bool {
+        const int64_t cbase = c_batch * (int64_t)f + c_off;
+        if constexpr (DBG) {
+            if (dbg.trace && c_off == 0 && col == 0 && (hi ? a1 : a0) > 0)
+                dbg.trace[c_batch + (hi ? 1 : 0)] = (int32_t)(w0 + (hi ? 1 : 0));
+        }
+        if (sync.every > 0 && c_off == 0 && ++batches % sync.every == 0) {
+            if (sync.leader) {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            } else if (sync.l1) {
+                asm volatile("buffer_inv sc0" ::: "memory");
+            }
+        }
+        for (int g = 0; g < H - D; g += D) { // look-ahead stays inside this chunk
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                const int x = g + j;
+                if (x >= a0)
+                    return false;
+                issue((j + D - 1) % D, aU, aV, aR, x + D - 1, a0, a1);
+                process(j, cbase + x);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < D; ++j) { // last group: look-ahead reaches into the next chunk
+            const int x = H - D + j;
+            if (x >= a0)
+                return false;
+            if (j == 0)
+                issue((j + D - 1) % D, aU, aV, aR, H - 1, a0, a1);
+            else
+                issue((j + D - 1) % D, bU, bV, bR, j - 1, b0, b1);
+            process(j, cbase + x);
+        }
+        if (b0 == 0)
+            return false;
+        c_batch = n_batch;
+        c_off = n_off;
+        advance(n_batch, n_off);
+        load_chunk(n_batch, n_off, aU, aV, aR, a0, a1);
+        return true;
+    };
+    for (;;) {
+        if (!chunk(cU, cV, cR, c0, c1, nU, nV, nR, n0, n1))
+            return;
+        if (!chunk(nU, nV, nR, n0, n1, cU, cV, cR, c0, c1))
             return;
     }
 }

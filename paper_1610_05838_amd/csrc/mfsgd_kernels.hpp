@@ -28,6 +28,21 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
     run_worker<KP, T, D, DBG, false, BUF>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
 }
 
+// The same with rows of 32 values: two workers per wavefront (run_worker_half),
+// wavefront h of the grid being workers 2 h and 2 h + 1.
+template <typename T, int D, bool DBG, bool BUF = false>
+__global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __restrict__ S, int64_t nnz, int64_t W,
+                                                                int f, T* __restrict__ P, T* __restrict__ Q, float lr,
+                                                                float lp, float lq, DebugSink dbg, int sync_every,
+                                                                int sync_l1, int nx)
+{
+    const int64_t wave = uniform64((int64_t)blockIdx.x * (kHogwildBlock / 64) + (threadIdx.x >> 6));
+    if (2 * wave >= W)
+        return;
+    const CacheSync sync{sync_every, (int)blockIdx.x < nx && (threadIdx.x >> 6) == 0, sync_l1 != 0};
+    run_worker_half<T, D, DBG, BUF>(S, nnz, W, wave, f, P, Q, lr, lp, lq, dbg, sync);
+}
+
 // Block-scheduled epoch: wavefront-update (section 3.2.3), and
 // batch-Hogwild! partitioned over the GPU's coherence domains.
 //
@@ -506,8 +521,24 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
     T* P = (T*)a.P;
     T* Q = (T*)a.Q;
     if (a.scheme == kSchemeHogwild) {
-        const int64_t blocks = (a.W + 3) / 4;
         const DebugSink dbg{a.visits, nullptr, a.trace_batch};
+        if constexpr (KP == 32) {
+            if (a.half) {
+                const int64_t blocks = ((a.W + 1) / 2 + 3) / 4;
+                if constexpr (sizeof(T) == 4 && !DBG) {
+                    if (a.buf) {
+                        hipLaunchKernelGGL((k_hogwild_half<T, D, false, true>), dim3((unsigned)blocks),
+                                           dim3(kHogwildBlock), 0, st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq,
+                                           dbg, a.sync_every, a.sync_l1, a.nx);
+                        return hipGetLastError();
+                    }
+                }
+                hipLaunchKernelGGL((k_hogwild_half<T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st,
+                                   a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
+                return hipGetLastError();
+            }
+        }
+        const int64_t blocks = (a.W + 3) / 4;
         constexpr bool kDword = sizeof(T) * Geo<KP>::E == 4; // one dword of a row per lane
         if constexpr (kDword && !DBG) {
             if (a.buf) {
@@ -591,23 +622,33 @@ static hipError_t launch_table_kp(const TableLaunch& a, hipStream_t st)
     }
 }
 
+// wavefronts of the one-address-space batch-Hogwild! kernel resident per CU
 template <int KP, typename T, int D>
-static int occupancy_t()
+static int occupancy_t(bool half)
 {
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild<KP, T, D, false>, kHogwildBlock, 0) != hipSuccess)
+    hipError_t e;
+    if constexpr (KP == 32) {
+        if (half)
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild_half<T, D, false>, kHogwildBlock, 0);
+        else
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild<KP, T, D, false>, kHogwildBlock, 0);
+    } else {
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild<KP, T, D, false>, kHogwildBlock, 0);
+    }
+    if (e != hipSuccess)
         return 0;
     return blocks * (kHogwildBlock / 64);
 }
 
 template <int KP, typename T>
-static int occupancy_kp(int depth)
+static int occupancy_kp(int depth, bool half)
 {
     switch (depth) {
-    case 1: return occupancy_t<KP, T, 1>();
-    case 2: return occupancy_t<KP, T, 2>();
-    case 4: return occupancy_t<KP, T, 4>();
-    case 8: return occupancy_t<KP, T, 8>();
+    case 1: return occupancy_t<KP, T, 1>(half);
+    case 2: return occupancy_t<KP, T, 2>(half);
+    case 4: return occupancy_t<KP, T, 4>(half);
+    case 8: return occupancy_t<KP, T, 8>(half);
     default: return 0;
     }
 }
@@ -652,14 +693,14 @@ struct Dispatch {
         default: return hipErrorInvalidValue;
         }
     }
-    static int occupancy(int KP, int depth)
+    static int occupancy(int KP, int depth, bool half)
     {
         switch (KP) {
-        case 32: return occupancy_kp<32, T>(depth);
-        case 64: return occupancy_kp<64, T>(depth);
-        case 128: return occupancy_kp<128, T>(depth);
-        case 256: return occupancy_kp<256, T>(depth);
-        case 512: return occupancy_kp<512, T>(depth);
+        case 32: return occupancy_kp<32, T>(depth, half);
+        case 64: return occupancy_kp<64, T>(depth, false);
+        case 128: return occupancy_kp<128, T>(depth, false);
+        case 256: return occupancy_kp<256, T>(depth, false);
+        case 512: return occupancy_kp<512, T>(depth, false);
         default: return 0;
         }
     }

@@ -7,7 +7,7 @@ hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st) { return Dispatch<hal
 
 hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st) { return Dispatch<half_t>::table_epoch(a, st); }
 
-int occupancy_f16(int KP, int depth) { return Dispatch<half_t>::occupancy(KP, depth); }
+int occupancy_f16(int KP, int depth, int half) { return Dispatch<half_t>::occupancy(KP, depth, half != 0); }
 
 int occupancy_blocked_f16(int KP, int depth, int threads)
 {

@@ -7,7 +7,7 @@ hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st) { return Dispatch<flo
 
 hipError_t table_epoch_f32(const TableLaunch& a, hipStream_t st) { return Dispatch<float>::table_epoch(a, st); }
 
-int occupancy_f32(int KP, int depth) { return Dispatch<float>::occupancy(KP, depth); }
+int occupancy_f32(int KP, int depth, int half) { return Dispatch<float>::occupancy(KP, depth, half != 0); }
 
 int occupancy_blocked_f32(int KP, int depth, int threads)
 {

@@ -34,6 +34,7 @@ struct EpochLaunch {
     int sync_l1;     // ... and whether the other wavefronts drop their CU's L1 then
     int nx;          // XCDs (one-address-space batch-Hogwild!: the first nx workgroups lead the flushes)
     int buf;         // every row offset of P and Q fits 31 bits: rows may be addressed through buffer descriptors
+    int half;        // batch-Hogwild! at KP = 32: two workers per wavefront
     // block-scheduled epochs
     const int64_t* bstart;
     int s;           // grid side
@@ -92,8 +93,9 @@ hipError_t epoch_f32(const EpochLaunch& a, hipStream_t st);
 hipError_t epoch_f16(const EpochLaunch& a, hipStream_t st);
 hipError_t table_epoch_f32(const TableLaunch& a, hipStream_t st);
 hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st);
-int occupancy_f32(int KP, int depth);
-int occupancy_f16(int KP, int depth);
+// wavefronts of the one-address-space batch-Hogwild! kernel per CU (half: two workers per wavefront)
+int occupancy_f32(int KP, int depth, int half);
+int occupancy_f16(int KP, int depth, int half);
 int occupancy_blocked_f32(int KP, int depth, int threads); // workgroups per CU
 int occupancy_blocked_f16(int KP, int depth, int threads);
 hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,

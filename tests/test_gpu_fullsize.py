@@ -31,7 +31,7 @@ def netflix(M, gen):
 
 def reset(M, **opts):
     o = dict(dtype=0, batch_f=256, workers=0, depth=2, team_waves=0, partition=2, hogwild_grid=0, balance=1,
-             sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0, wave_launch=0, table_grid=256,
+             sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0, wave_launch=0, half_waves=1, table_grid=256,
              table_workers=0)
     o.update(opts)
     for k, v in o.items():

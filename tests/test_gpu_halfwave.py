@@ -1,0 +1,181 @@
+"""Two batch-Hogwild! workers per wavefront at k <= 32 (option half_waves).
+
+A row of 32 values fills half of a 64-lane wavefront, so the one-address-space
+batch-Hogwild! kernel runs one worker per half.  Checks, through the C ABI:
+
+* a lone worker computes the same bits as the one-worker-per-wavefront kernel
+  (its 32-lane dot product adds the same terms in the same order) and matches
+  the serial oracle (section 3.2.2 with W = 1 is the serial order);
+* W workers whose batches touch disjoint rows and columns (batch b uses only
+  the rows of group b mod W) do not interact, so the result is the serial
+  oracle's whatever the interleaving, bit-identical to the one-per-wavefront
+  kernel; odd W leaves the upper half of the last wavefront idle, and ragged
+  sizes end a half's sequence mid-chunk or mid-batch;
+* the schedule: batch b is run by worker b mod W, every sample exactly once.
+Tolerances as in the other parity tests: max-abs 1e-4 (binary32) and 2e-2
+(binary16) against the binary64 oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {np.float32: 1e-4, np.float16: 2e-2}
+DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=2, team_waves=0, partition=0, hogwild_grid=0, balance=1,
+                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0,
+                wave_launch=0, half_waves=1, table_grid=256, table_workers=0)
+
+
+@pytest.fixture(scope="module")
+def M():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1610_05838_amd import mfsgd
+    mfsgd.lib()
+    yield mfsgd
+    mfsgd.finalize()
+
+
+def run(M, S, m, n, k, seed, dtype, epochs=1, **opts):
+    o = dict(DEFAULTS)
+    o["dtype"] = 1 if dtype == np.float16 else 0
+    o.update(opts)
+    for key, val in o.items():
+        M.set_option(key, val)
+    M.init(m, n, k, seed)
+    dS = M.samples_to_device(S)
+    for _ in range(epochs):
+        M.epoch(dS, 0.01, 0.05, 0.04, "hogwild")
+    P, Q = M.get_factors(m, n, k)
+    return P.cpu().numpy().astype(dtype), Q.cpu().numpy().astype(dtype)
+
+
+def serial(S, m, n, k, seed, dtype, epochs=1):
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for _ in range(epochs):
+        oracle.epoch_serial(Po, Qo, S, 0.01, 0.05, 0.04)
+    return Po, Qo
+
+
+def maxabs(a, b):
+    return float(np.max(np.abs(a.astype(np.float64) - b.astype(np.float64)))) if a.size else 0.0
+
+
+def bits(a):
+    return a.view(np.uint32 if a.dtype == np.float32 else np.uint16)
+
+
+def grouped_samples(rng, W, f, nnz, mu, nv):
+    """Batch b of f consecutive samples draws its user from [g mu, (g+1) mu)
+    and its item from [g nv, (g+1) nv), g = b mod W: the workers of
+    batch-Hogwild! with W workers then share no row and no column."""
+    a = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    g = (np.arange(nnz) // f) % W
+    a["u"] = g * mu + rng.integers(0, mu, nnz)
+    a["v"] = g * nv + rng.integers(0, nv, nnz)
+    a["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+    return a, W * mu, W * nv
+
+
+@pytest.mark.parametrize("depth", [1, 2, 4, 8])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("k", [1, 20, 32])
+def test_lone_worker_same_bits_as_full_wavefront(M, depth, dtype, k):
+    rng = np.random.default_rng(100 * depth + k)
+    for m, n, nnz in ((7, 5, 2001), (400, 300, 6037)):  # 7 x 5: consecutive samples share rows all the time
+        S = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+        S["u"] = rng.integers(0, m, nnz)
+        S["v"] = rng.integers(0, n, nnz)
+        S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+        seed = 5 + k
+        Ph, Qh = run(M, S, m, n, k, seed, dtype, workers=1, depth=depth, half_waves=1)
+        Pf, Qf = run(M, S, m, n, k, seed, dtype, workers=1, depth=depth, half_waves=0)
+        assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf)), (m, n)
+        Po, Qo = serial(S, m, n, k, seed, dtype)
+        assert maxabs(Ph, Po) <= TOL[dtype] and maxabs(Qh, Qo) <= TOL[dtype], (m, n)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("W,f,nnz", [
+    (2, 256, 20 * 256),            # both halves of one wavefront, whole batches
+    (2, 64, 37 * 64 + 45),         # ragged: the array ends inside the upper half's batch
+    (3, 256, 11 * 256 + 200),      # odd: the second wavefront's upper half idles
+    (5, 128, 23 * 128 + 17),       # last batch partial and owned by a lower half
+    (8, 64, 8 * 64 * 3 + 64 + 31), # the last wavefronts run one batch fewer
+])
+def test_disjoint_workers_equal_serial(M, dtype, W, f, nnz):
+    rng = np.random.default_rng(W * 7919 + nnz)
+    S, m, n = grouped_samples(rng, W, f, nnz, 6, 4)
+    k, seed = 32, 41 + W
+    for depth in (1, 2, 8):
+        Ph, Qh = run(M, S, m, n, k, seed, dtype, epochs=2, workers=W, batch_f=f, depth=depth, half_waves=1)
+        Pf, Qf = run(M, S, m, n, k, seed, dtype, epochs=2, workers=W, batch_f=f, depth=depth, half_waves=0)
+        assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf)), depth
+        Po, Qo = serial(S, m, n, k, seed, dtype, epochs=2)
+        assert maxabs(Ph, Po) <= TOL[dtype] and maxabs(Qh, Qo) <= TOL[dtype], depth
+
+
+@pytest.mark.parametrize("k", [16, 32])
+@pytest.mark.parametrize("W", [1, 2, 7, 1000, 0])
+def test_schedule_and_coverage(M, k, W):
+    rng = np.random.default_rng(W + k)
+    m, n, nnz, seed, f = 3000, 2000, 300_017, 9, 256
+    S = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    S["u"] = rng.integers(0, m, nnz)
+    S["v"] = rng.integers(0, n, nnz)
+    S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+    for key, val in dict(DEFAULTS, debug=3, workers=W).items():
+        M.set_option(key, val)
+    M.init(m, n, k, seed)
+    M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
+    assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+    nb = (nnz + f - 1) // f
+    trace = M.debug_trace(nb).cpu().numpy()
+    if W == 0:  # the default: two workers per resident wavefront, fewer if batches run out
+        Wd = min(2 * M.get_option("resident_waves"), nb)
+        assert np.array_equal(trace, oracle.hogwild_batch_owner(nnz, f, Wd))
+    else:
+        assert np.array_equal(trace, oracle.hogwild_batch_owner(nnz, f, min(W, nb)))
+
+
+@pytest.mark.parametrize("nnz", [1, 5, 31, 32, 33, 255, 257])
+def test_tiny_arrays(M, nnz):
+    rng = np.random.default_rng(nnz)
+    m, n, k, seed = 9, 6, 32, 3
+    S = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    S["u"] = rng.integers(0, m, nnz)
+    S["v"] = rng.integers(0, n, nnz)
+    S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+    for W in (1, 2, 3):
+        P, Q = run(M, S, m, n, k, seed, np.float32, workers=W, batch_f=64)
+        if W == 1 or nnz <= 64:  # a single batch: one worker runs everything
+            Po, Qo = serial(S, m, n, k, seed, np.float32)
+            assert maxabs(P, Po) <= 1e-4 and maxabs(Q, Qo) <= 1e-4, W
+
+
+def test_two_workers_rmse_gap(M, gen):
+    """Both halves of one wavefront as two batch-Hogwild! workers that do
+    share rows (the tiny workload's model and density on a 4000 x 2000 grid):
+    after five epochs the test RMSE is within the binary32 Hogwild! tolerance
+    of the serial oracle's (workers far below min(m, n), the condition under
+    which Hogwild! behaves like serial SGD)."""
+    w = gen.workload("tiny", m=4000, n=2000, ntrain=49_500 * 16, ntest=500 * 16, seed=gen.SEED_BASE + 11)
+    S, T = gen.make(w)
+    m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
+    assert k <= 32
+    for key, val in dict(DEFAULTS, workers=2).items():
+        M.set_option(key, val)
+    M.init(m, n, k, seed)
+    dS, dT = M.samples_to_device(S), M.samples_to_device(T)
+    for _ in range(5):
+        M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    got = M.rmse(dT)
+    Po, Qo = oracle.init_factors(m, n, k, seed, np.float32)
+    for _ in range(5):
+        oracle.epoch_serial(Po, Qo, S, w["lr"], w["lam"], w["lam"])
+    want = oracle.rmse(Po, Qo, T)
+    print(f"two half-wavefront workers rmse {got:.6f} oracle {want:.6f}")
+    assert abs(got - want) <= 1e-3

@@ -12,7 +12,7 @@ pytestmark = pytest.mark.gpu
 
 TOL = {np.float32: 1e-4, np.float16: 2e-2}
 DEFAULTS = dict(dtype=0, batch_f=256, workers=0, depth=2, team_waves=0, partition=2, hogwild_grid=0, balance=2,
-                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, stage_samples=1 << 25, debug=0)
+                sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, stage_samples=1 << 25, half_waves=1, debug=0)
 
 
 @pytest.fixture(scope="module")
