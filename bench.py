@@ -345,7 +345,7 @@ def main():
     variant = [x for i, x in enumerate(variant) if x not in drop and (i == 0 or variant[i - 1] not in drop)]
     traffic = measured_traffic(key, variant)
     out = {
-        "metric": "SGD updates/sec and achieved HBM GB/s (% of peak) at k=128, 1 MI355X",
+        "metric": f"SGD updates/sec and achieved HBM GB/s (% of peak) at k={w['k']}, 1 MI355X",
         "value": value,
         "unit": "updates/s",
         "n_gpus": 1,
