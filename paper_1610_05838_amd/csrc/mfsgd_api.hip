@@ -997,6 +997,9 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
     a.pool = want == 1 ? 0 : 1;
     a.wg_waves = waves;
     a.sink = skip_stores(pl) ? c.sink : nullptr;
+    // pooled teams claim two batches per wavefront at k <= 32 (one-wavefront
+    // teams keep their blocks' serial order, store-skipping epochs their sinks)
+    a.half = half_wave_workers(c.KP) && want != 1 && !a.sink ? 1 : 0;
     return MFSGD_OK;
 }
 

@@ -91,7 +91,11 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // last batch (taken before the column's ticket moves on).  In every column,
 // the block of wave w+1 must be claimed only after the block of wave w was
 // completed; the host checks that from the stamps.
-template <int KP, typename T, int D, bool DBG, bool SKIP>
+//
+// HALF (rows of 32 values, KP = 32): a wavefront claims two consecutive
+// batches of the block at once and runs them as two workers, one per half
+// (run_worker_half); the block's finished count advances by the batches run.
+template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, const int32_t* __restrict__ tmap,
                                                  const int32_t* __restrict__ xteams, int nx, int pool, int free_run,
@@ -100,6 +104,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
                                                  uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
                                                  DebugSink dbg, int32_t* trace, T* __restrict__ sink)
 {
+    static_assert(!HALF || (KP == 32 && !SKIP), "half-wavefront workers: rows of 32 values, no store redirection");
+    constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per claim
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
     const int tm = tmap[blockIdx.x];
     if (tm < 0)
@@ -169,7 +175,7 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
         const uint32_t nb = (uint32_t)((hi - lo + f - 1) / f);
         uint32_t idx = 0;
         if (lane == 0)
-            idx = __hip_atomic_fetch_add(claim + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            idx = __hip_atomic_fetch_add(claim + tw, kClaim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         idx = __builtin_amdgcn_readfirstlane(idx);
         if (idx >= nb) {
             // nothing left to claim in this block: move the team's cursor on;
@@ -206,21 +212,26 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             entered = tw;
         }
         const int64_t b0 = lo + (int64_t)idx * f;
-        const int64_t cnt = hi - b0 < f ? hi - b0 : f;
+        const int64_t span = (int64_t)kClaim * f;
+        const int64_t cnt = hi - b0 < span ? hi - b0 : span;
+        const uint32_t ran = cnt > f ? 2u : 1u; // batches this claim covers
         DebugSink blk = dbg;
         blk.trace = nullptr;
         if (blk.orig)
             blk.orig += b0;
-        run_worker<KP, T, D, DBG, SKIP>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk, CacheSync{0, false, false},
-                                        my_sink);
+        if constexpr (HALF)
+            run_worker_half<T, D, DBG>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk);
+        else
+            run_worker<KP, T, D, DBG, SKIP>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk, CacheSync{0, false, false},
+                                            my_sink);
         // this wavefront's stores have reached the XCD's L2 before it counts
-        // the batch as finished
+        // the batches as finished
         __builtin_amdgcn_s_waitcnt(0);
         uint32_t done = 0;
         if (lane == 0)
-            done = __hip_atomic_fetch_add(fin + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            done = __hip_atomic_fetch_add(fin + tw, ran, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         done = __builtin_amdgcn_readfirstlane(done);
-        if (done == nb - 1) {
+        if (done + ran == nb) {
             // last batch of the block: every batch's stores are in this XCD's
             // L2; write it back, then pass the column on
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -436,6 +447,13 @@ static int occupancy_blocked_t(int threads)
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&plain, k_blocked<KP, T, D, false, false>, threads, 0) !=
             hipSuccess)
         return 0;
+    if constexpr (KP == 32) {
+        int half = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&half, k_blocked<KP, T, D, false, false, true>, threads, 0) !=
+            hipSuccess)
+            return 0;
+        plain = half < plain ? half : plain;
+    }
     return blocks < plain ? blocks : plain;
 }
 
@@ -556,6 +574,15 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
                            a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, dbg, a.trace_wave);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
+        if constexpr (KP == 32) {
+            if (a.half && !a.sink) {
+                hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool,
+                                   a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
+                                   a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr);
+                return hipGetLastError();
+            }
+        }
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,

@@ -179,3 +179,101 @@ def test_two_workers_rmse_gap(M, gen):
     want = oracle.rmse(Po, Qo, T)
     print(f"two half-wavefront workers rmse {got:.6f} oracle {want:.6f}")
     assert abs(got - want) <= 1e-3
+
+
+# ---------------------------------------------------------------------------- block-scheduled kernel
+def disjoint_block_samples(rng, s, f, G, gu, gv):
+    """An s x s grid (equal index ranges) in which batch j of block (t, c)
+    draws its users from sub-range c G + j of row block t and its items from
+    sub-range j of column block c.  Every user then belongs to one batch, and
+    an item's batches lie in different blocks of its column, which the
+    column tickets order: batches that may run at the same time (those of one
+    block, and those of a team's consecutive blocks) touch disjoint rows, so
+    any run of the schedule equals the serial update in the schedule's block
+    order.  Blocks hold 0..G batches of f samples, the last one ragged; the
+    array lists the blocks in random order, each block's samples in batch
+    order."""
+    m, n = s * s * G * gu, s * G * gv
+    parts = []
+    for t in range(s):
+        for c in range(s):
+            nb = int(rng.integers(0, G + 1))
+            for j in range(nb):
+                cnt = f if j < nb - 1 else int(rng.integers(1, f + 1))
+                a = np.zeros(cnt, dtype=oracle.SAMPLE_DTYPE)
+                a["u"] = (t * s + c) * G * gu + j * gu + rng.integers(0, gu, cnt)
+                a["v"] = c * G * gv + j * gv + rng.integers(0, gv, cnt)
+                a["r"] = rng.uniform(1.0, 5.0, cnt).astype(np.float32)
+                parts.append((t * s + c, j, a))
+    order = rng.permutation(s * s)
+    rank = np.empty(s * s, dtype=np.int64)
+    rank[order] = np.arange(s * s)
+    parts.sort(key=lambda p: (rank[p[0]], p[1]))
+    return np.concatenate([p[2] for p in parts]), m, n
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("scheme,s", [("wavefront", 4), ("wavefront", 8), ("hogwild", 8)])
+def test_block_scheduled_pairs_equal_schedule_order(M, dtype, scheme, s):
+    """Pooled teams at k = 32 claim two batches per wavefront and run one per
+    half; on blocks whose batches commute the result is the oracle's update in
+    the wavefront block order (section 3.2.3), and the same bits as one batch
+    per wavefront."""
+    rng = np.random.default_rng(s * 31 + (scheme == "hogwild"))
+    f = 64
+    S, m, n = disjoint_block_samples(rng, s, f, 6, 3, 2)
+    k, seed = 32, 123 + s
+    opts = dict(batch_f=f, balance=0, partition=1 if scheme == "hogwild" else 0, hogwild_grid=s, skip_stores=0)
+    res = {}
+    for half in (1, 0):
+        o = dict(DEFAULTS, dtype=1 if dtype == np.float16 else 0, half_waves=half, **opts)
+        for key, val in o.items():
+            M.set_option(key, val)
+        M.init(m, n, k, seed)
+        dS = M.samples_to_device(S)
+        if scheme == "wavefront":
+            M.plan(dS, s)
+        else:
+            assert M.get_option("partitioned") == 1
+        for _ in range(2):
+            M.epoch(dS, 0.01, 0.05, 0.04, scheme)
+        P, Q = M.get_factors(m, n, k)
+        res[half] = (P.cpu().numpy().astype(dtype), Q.cpu().numpy().astype(dtype))
+    (Ph, Qh), (Pf, Qf) = res[1], res[0]
+    assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf))
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(2):
+        oracle.epoch_wavefront(Po, Qo, S, 0.01, 0.05, 0.04, s, seed, t, balanced=False)
+    assert maxabs(Ph, Po) <= TOL[dtype] and maxabs(Qh, Qo) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("scheme,s,opts", [
+    ("wavefront", 32, {}), ("wavefront", 8, {"balance": 0}), ("hogwild", 8, {"partition": 1}),
+])
+def test_block_scheduled_pairs_coverage_and_handover(M, gen, scheme, s, opts):
+    """Race check with two batches per claim (k = 32, pooled teams, Zipf
+    blocks): every sample once, the oracle's column orders, and in every
+    column each wave's block claimed only after the previous wave's block
+    completed (claim and completion stamps of one event counter)."""
+    w = gen.workload("netflix", m=30_000, n=4_000, ntrain=800_000, ntest=0)
+    S = gen.draw(w, 0, w["ntrain"])
+    for key, val in dict(DEFAULTS, **{"partition": 2, "debug": 3, "skip_stores": 0, **opts}).items():
+        M.set_option(key, val)
+    M.init(w["m"], w["n"], 32, w["seed"])
+    dS = M.samples_to_device(S)
+    if scheme != "hogwild":
+        M.plan(dS, s)
+    for t in range(2):
+        M.epoch(dS, 0.002, 0.01, 0.01, scheme)
+        assert bool((M.debug_visits(len(S)) == 1).all().item())
+        tr = M.debug_trace(3 * s * s).cpu().numpy()
+        assert np.array_equal(tr[:s * s].reshape(s, s), oracle.wavefront_sigma(w["seed"], t, s))
+        cols = tr[:s * s].reshape(s, s)
+        st = tr[s * s:3 * s * s].view(np.uint32).reshape(s, s, 2).astype(np.int64)
+        assert np.all(st[:, :, 0] < st[:, :, 1])
+        team_of = np.empty((s, s), dtype=np.int64)
+        for tm in range(s):
+            team_of[cols[tm], np.arange(s)] = tm
+        for c in range(s):
+            prev, nxt = team_of[c, :-1], team_of[c, 1:]
+            assert np.all(st[nxt, np.arange(1, s), 0] > st[prev, np.arange(s - 1), 1]), c
