@@ -185,8 +185,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  run (the final values are the same).  0 never, 1 always,
  *                  2 (default) when one user or one item holds more than
  *                  half of the samples of its row or column block (many
- *                  wavefronts then update one row at once).  Epochs with
- *                  debug output never skip.
+ *                  wavefronts then update one row at once), except in
+ *                  partitioned batch-Hogwild! at k <= 32 with "half_waves"
+ *                  on.  Epochs with debug output never skip.
  *   "stage_samples" samples per chunk of mfsgd_epoch_staged (default 2^25,
  *                  402 MB per buffer; three device buffers, and three
  *                  pinned host buffers for pageable arrays).
@@ -196,13 +197,16 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  waves, no tickets), a cross-check of the ticketed kernel
  *                  whose factors it reproduces bit for bit; 0 (default) the
  *                  persistent ticketed kernel.
- *   "half_waves"   one-address-space batch-Hogwild! with k <= 32: 1
- *                  (default) runs two workers per wavefront, one per half
- *                  of its 64 lanes (a row of 32 values fills a half), so
- *                  "workers" and the default worker count are then counted
- *                  in half-wavefronts; 0 one worker per wavefront, whose
- *                  upper 32 lanes idle.  A lone worker computes the same
- *                  bits either way.
+ *   "half_waves"   batch-Hogwild! with k <= 32: 1 (default) runs two workers
+ *                  per wavefront, one per half of its 64 lanes (a row of 32
+ *                  values fills a half).  In one address space "workers"
+ *                  and the default worker count are then counted in
+ *                  half-wavefronts; partitioned (teams of more than one
+ *                  wavefront), a wavefront claims two batches of its open
+ *                  block at once, one per half, instead of skipping stores
+ *                  (unless "skip_stores" is 1).  0: one worker per
+ *                  wavefront, whose upper 32 lanes idle.  A lone worker
+ *                  computes the same bits either way.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and

@@ -997,9 +997,7 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
     a.pool = want == 1 ? 0 : 1;
     a.wg_waves = waves;
     a.sink = skip_stores(pl) ? c.sink : nullptr;
-    // pooled teams claim two batches per wavefront at k <= 32 (one-wavefront
-    // teams keep their blocks' serial order, store-skipping epochs their sinks)
-    a.half = half_wave_workers(c.KP) && want != 1 && !a.sink ? 1 : 0;
+    a.half = 0;
     return MFSGD_OK;
 }
 
@@ -1099,6 +1097,15 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.bstart = pl->bstart;
         a.s = s;
         CHK(team_layout(*pl, want, a));
+        if (hog && want != 1 && half_wave_workers(c.KP) && g_opt.skip_stores != 1) {
+            // Partitioned batch-Hogwild! at k <= 32: pooled wavefronts claim
+            // two batches at a time and run one per half, in place of skipped
+            // stores (measured faster on the Netflix shape at k = 32; pairs
+            // were slower for wavefront-update, which keeps one batch per
+            // wavefront, as do one-wavefront teams, whose blocks run in order).
+            a.half = 1;
+            a.sink = nullptr;
+        }
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;

@@ -213,17 +213,19 @@ def disjoint_block_samples(rng, s, f, G, gu, gv):
 
 
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-@pytest.mark.parametrize("scheme,s", [("wavefront", 4), ("wavefront", 8), ("hogwild", 8)])
-def test_block_scheduled_pairs_equal_schedule_order(M, dtype, scheme, s):
-    """Pooled teams at k = 32 claim two batches per wavefront and run one per
-    half; on blocks whose batches commute the result is the oracle's update in
-    the wavefront block order (section 3.2.3), and the same bits as one batch
-    per wavefront."""
-    rng = np.random.default_rng(s * 31 + (scheme == "hogwild"))
+@pytest.mark.parametrize("s,skip", [(4, 0), (8, 0), (8, 2), (16, 0)])
+def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
+    """Partitioned batch-Hogwild! at k = 32: pooled wavefronts claim two
+    batches at a time and run one per half (also where skipped stores would
+    be chosen); on blocks whose concurrently runnable batches commute the
+    result is the oracle's update in the wavefront block order (section
+    3.2.3), and the same bits as one batch per wavefront."""
+    scheme = "hogwild"
+    rng = np.random.default_rng(s * 31 + skip)
     f = 64
     S, m, n = disjoint_block_samples(rng, s, f, 6, 3, 2)
     k, seed = 32, 123 + s
-    opts = dict(batch_f=f, balance=0, partition=1 if scheme == "hogwild" else 0, hogwild_grid=s, skip_stores=0)
+    opts = dict(batch_f=f, balance=0, partition=1, hogwild_grid=s, skip_stores=skip)
     res = {}
     for half in (1, 0):
         o = dict(DEFAULTS, dtype=1 if dtype == np.float16 else 0, half_waves=half, **opts)
@@ -248,13 +250,15 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, scheme, s):
 
 
 @pytest.mark.parametrize("scheme,s,opts", [
-    ("wavefront", 32, {}), ("wavefront", 8, {"balance": 0}), ("hogwild", 8, {"partition": 1}),
+    ("hogwild", 8, {"partition": 1}), ("hogwild", 16, {"partition": 1, "hogwild_grid": 16}),
+    ("wavefront", 32, {}),
 ])
 def test_block_scheduled_pairs_coverage_and_handover(M, gen, scheme, s, opts):
-    """Race check with two batches per claim (k = 32, pooled teams, Zipf
-    blocks): every sample once, the oracle's column orders, and in every
-    column each wave's block claimed only after the previous wave's block
-    completed (claim and completion stamps of one event counter)."""
+    """Race check with two batches per claim (partitioned batch-Hogwild! at
+    k = 32, pooled teams, Zipf blocks; wavefront-update, which keeps one batch
+    per claim, alongside): every sample once, the oracle's column orders, and
+    in every column each wave's block claimed only after the previous wave's
+    block completed (claim and completion stamps of one event counter)."""
     w = gen.workload("netflix", m=30_000, n=4_000, ntrain=800_000, ntest=0)
     S = gen.draw(w, 0, w["ntrain"])
     for key, val in dict(DEFAULTS, **{"partition": 2, "debug": 3, "skip_stores": 0, **opts}).items():
