@@ -271,7 +271,7 @@ def main():
     resident = mfsgd.get_option("resident_waves")
     partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged
     kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
-    if kernel == "k_hogwild" and w["k"] <= 32 and mfsgd.get_option("half_waves"):
+    if kernel == "k_hogwild" and mfsgd.get_option("half_workers"):
         kernel = "k_hogwild_half"
     grid_s = args.grid_s or w.get("grid_s", 32)
     if args.scheme == "table":

@@ -197,16 +197,20 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  waves, no tickets), a cross-check of the ticketed kernel
  *                  whose factors it reproduces bit for bit; 0 (default) the
  *                  persistent ticketed kernel.
- *   "half_waves"   batch-Hogwild! with k <= 32: 1 (default) runs two workers
- *                  per wavefront, one per half of its 64 lanes (a row of 32
- *                  values fills a half).  In one address space "workers"
- *                  and the default worker count are then counted in
- *                  half-wavefronts; partitioned (teams of more than one
- *                  wavefront), a wavefront claims two batches of its open
- *                  block at once, one per half, instead of skipping stores
- *                  (unless "skip_stores" is 1).  0: one worker per
- *                  wavefront, whose upper 32 lanes idle.  A lone worker
- *                  computes the same bits either way.
+ *   "half_waves"   two batch-Hogwild! workers per wavefront, one per half
+ *                  of its 64 lanes, each lane holding (padded k)/32 values.
+ *                  1 (default): at k <= 32 (a row of 32 values fills a
+ *                  half); 2: in one address space at every width of
+ *                  at most 16 bytes per lane (binary32 k <= 128, binary16
+ *                  k <= 256); 0: never (at k <= 32 the upper 32 lanes then
+ *                  idle).  In one address space "workers" and the default
+ *                  worker count are then counted in half-wavefronts;
+ *                  partitioned (teams of more than one wavefront, k <= 32),
+ *                  a wavefront claims two batches of its open block at
+ *                  once, one per half, instead of skipping stores (unless
+ *                  "skip_stores" is 1).  At k <= 32 a lone worker computes
+ *                  the same bits either way; at wider rows its lane sums
+ *                  run in another order.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and
@@ -221,6 +225,8 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs the
  * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
  * "partitioned" (whether batch-Hogwild! runs partitioned for this model),
+ * "half_workers" (whether its one-address-space form runs two workers per
+ * wavefront for this model),
  * "table_blocks" (non-empty blocks of the last global-table plan, 0 before one),
  * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
  * block-scheduled kernel), "teams_grid" (workgroups of the last

@@ -289,11 +289,23 @@ int padded_width(int k)
 }
 
 // Whether one-address-space batch-Hogwild! runs two workers per wavefront.
-bool half_wave_workers(int KP) { return KP == 32 && g_opt.half_waves != 0; }
+// By default (half_waves = 1) at KP = 32, where one worker per wavefront
+// leaves half of the lanes idle.  Wider rows (half_waves = 2: every width of
+// at most 16 bytes per half-wavefront lane) were no faster per epoch on the
+// Netflix shape except binary16 at KP = 64, and twice the workers converge
+// worse per epoch, so they are not the default.  0: never.
+bool half_wave_workers(int KP, int dtype)
+{
+    if (g_opt.half_waves == 0)
+        return false;
+    if (g_opt.half_waves == 2)
+        return (int64_t)KP * (int64_t)elem_size(dtype) <= 16 * 32;
+    return KP == 32;
+}
 
 int occupancy_waves(int KP, int dtype, int depth)
 {
-    const int half = half_wave_workers(KP) ? 1 : 0;
+    const int half = half_wave_workers(KP, dtype) ? 1 : 0;
     return dtype == MFSGD_FP16 ? occupancy_f16(KP, depth, half) : occupancy_f32(KP, depth, half);
 }
 
@@ -377,7 +389,7 @@ const OptSpec kOpts[] = {
     {"skip_stores", &Options::skip_stores, 0, 2, "skip_stores must be 0, 1 or 2"},
     {"stage_samples", &Options::stage_samples, 64, int64_t(1) << 31, "stage_samples must be in [64, 2^31]"},
     {"wave_launch", &Options::wave_launch, 0, 1, "wave_launch must be 0 or 1"},
-    {"half_waves", &Options::half_waves, 0, 1, "half_waves must be 0 or 1"},
+    {"half_waves", &Options::half_waves, 0, 2, "half_waves must be 0, 1 or 2"},
     {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
     {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
@@ -414,7 +426,8 @@ int get_option_impl(const char* key, int64_t* value)
         }
     const bool ro = !std::strcmp(key, "resident_waves") || !std::strcmp(key, "xcds") || !std::strcmp(key, "cus") ||
                     !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
-                    !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks");
+                    !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks") ||
+                    !std::strcmp(key, "half_workers");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
@@ -423,6 +436,8 @@ int get_option_impl(const char* key, int64_t* value)
         *value = (int64_t)g.cus * occupancy_waves(g.KP, g.dtype, (int)g_opt.depth);
     else if (!std::strcmp(key, "xcds"))
         *value = g.nx;
+    else if (!std::strcmp(key, "half_workers"))
+        *value = half_wave_workers(g.KP, g.dtype) ? 1 : 0;
     else if (!std::strcmp(key, "blocked_per_cu"))
         *value = occupancy_blocked(g.KP, g.dtype, (int)g_opt.depth, 256);
     else if (!std::strcmp(key, "partitioned"))
@@ -1061,11 +1076,11 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);
             if (per_cu <= 0)
                 return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
-            W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP) ? 2 : 1);
+            W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP, c.dtype) ? 2 : 1);
         }
         W = std::min(W, nbatch);
         a.scheme = kSchemeHogwild;
-        a.half = half_wave_workers(c.KP) ? 1 : 0;
+        a.half = half_wave_workers(c.KP, c.dtype) ? 1 : 0;
         a.S = (const Sample*)samples;
         a.W = W;
         a.sync_every = (int)g_opt.sync_every;
@@ -1097,7 +1112,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.bstart = pl->bstart;
         a.s = s;
         CHK(team_layout(*pl, want, a));
-        if (hog && want != 1 && half_wave_workers(c.KP) && g_opt.skip_stores != 1) {
+        if (hog && want != 1 && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1) {
             // Partitioned batch-Hogwild! at k <= 32: pooled wavefronts claim
             // two batches at a time and run one per half, in place of skipped
             // stores (measured faster on the Netflix shape at k = 32; pairs
@@ -1236,9 +1251,9 @@ int epoch_staged_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float 
         const int per_cu = occupancy_waves(c.KP, c.dtype, a.depth);
         if (per_cu <= 0)
             return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
-        W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP) ? 2 : 1);
+        W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP, c.dtype) ? 2 : 1);
     }
-    a.half = half_wave_workers(c.KP) ? 1 : 0;
+    a.half = half_wave_workers(c.KP, c.dtype) ? 1 : 0;
     if (dbg & 1) {
         CHK(grow(&c.visits, &c.visits_cap, nnz, "visit counters"));
         c.visits_n = nnz;

@@ -560,11 +560,13 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
 }
 
 // ---------------------------------------------------------------------------
-// Two batch-Hogwild! workers per wavefront, for rows of 32 values (KP = 32),
-// where a one-worker wavefront would leave half of its lanes idle.
+// Two batch-Hogwild! workers per wavefront.  At KP = 32 a one-worker
+// wavefront would leave half of its lanes idle; at wider rows each lane of a
+// half holds KP/32 values (at most 16 bytes), so one memory instruction moves
+// the rows of two samples.
 //
 // Lanes 0-31 are worker 2 h and lanes 32-63 worker 2 h + 1 of the W workers
-// (h = the wavefront's index); each half holds one value of a row per lane and
+// (h = the wavefront's index); each half holds a row across its 32 lanes and
 // runs the sequence of run_worker's worker (batches b = worker, worker+W, ...
 // of f consecutive samples, in array order) with the same in-flight window,
 // forwarding and arithmetic.  The two halves step through their sequences
@@ -574,22 +576,27 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
 // f further on).  A position past a half's count loads row 0 and stores
 // nothing.  Each half's dot product is a 32-lane sum; with one active half it
 // adds the same terms in the same order as run_worker's 64-lane sum (whose
-// idle lanes add zeros), so a lone worker computes the same bits either way.
+// idle lanes add zeros) at KP = 32, so a lone worker computes the same bits
+// either way there; wider rows sum their products in another order.
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool DBG, bool BUF = false>
+template <int KP, typename T, int D, bool DBG, bool BUF = false>
 __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t wave,
                                                 int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
                                                 float lq, const DebugSink dbg,
                                                 const CacheSync sync = CacheSync{0, false, false})
 {
-    constexpr int KP = 32;
-    constexpr int H = 32; // positions per chunk and half
-    static_assert(!BUF || sizeof(T) == 4, "buffer rows: one dword per lane");
+    constexpr int H = 32;      // positions per chunk and half; lanes per half
+    constexpr int E = KP / H;  // values per lane
+    typedef Row<T, E> R;
+    typedef typename VecT<T, E>::type V;
+    static_assert(KP % H == 0 && sizeof(V) <= 16, "rows of 32 to 512 values, at most 16 bytes per lane");
+    static_assert(!BUF || sizeof(V) == 4, "buffer rows: one dword per lane");
     static_assert(H % D == 0 && D <= 16, "depth must divide 32");
 
     const int lane = lane_id();
     const bool hi = lane >= H;           // lanes 32-63
-    const int col = lane & (H - 1);       // value of a row held by this lane
+    const int hl = lane & (H - 1);        // lane within the half
+    const int col = hl * E;               // first value of a row held by this lane
     const int64_t w0 = 2 * wave;          // worker of lanes 0-31
     const bool two = w0 + 1 < W;          // lanes 32-63 are a worker too
     const Buf bp(P), bq(Q);
@@ -617,7 +624,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
         c0 = count(s0);
         c1 = two ? count(s0 + f) : 0;
         const int mine = hi ? c1 : c0;
-        const int64_t i = s0 + (hi ? f : 0) + (col < mine ? col : 0);
+        const int64_t i = s0 + (hi ? f : 0) + (hl < mine ? hl : 0);
         const Sample* sp = S + (mine > 0 ? i : 0);
         cu = __builtin_nontemporal_load(&sp->u);
         cv = __builtin_nontemporal_load(&sp->v);
@@ -634,12 +641,12 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
 
     int su[D], sv[D], hu[D], hv[D];
     float sr[D];
-    T sp[D], sq[D], hp[D], hq[D];
+    V sp[D], sq[D], hp[D], hq[D];
 #pragma unroll
     for (int d = 0; d < D; ++d) {
         su[d] = sv[d] = hu[d] = hv[d] = -1;
         sr[d] = 0.f;
-        sp[d] = sq[d] = hp[d] = hq[d] = T{};
+        sp[d] = sq[d] = hp[d] = hq[d] = V{};
     }
 
     // request the rows of each half's sample at position xl of a chunk
@@ -654,11 +661,11 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
         sv[slot] = ok ? v : -1;
         sr[slot] = __int_as_float(hi ? r1 : r0);
         if constexpr (BUF) {
-            sp[slot] = bp.template ld<T>(cb + (uint32_t)(ok ? u : 0) * kRowBytes, 0);
-            sq[slot] = bq.template ld<T>(cb + (uint32_t)(ok ? v : 0) * kRowBytes, 0);
+            sp[slot] = bp.template ld<V>(cb + (uint32_t)(ok ? u : 0) * kRowBytes, 0);
+            sq[slot] = bq.template ld<V>(cb + (uint32_t)(ok ? v : 0) * kRowBytes, 0);
         } else {
-            sp[slot] = P[(int64_t)(ok ? u : 0) * KP + col];
-            sq[slot] = Q[(int64_t)(ok ? v : 0) * KP + col];
+            sp[slot] = R::ld(P + (int64_t)(ok ? u : 0) * KP + col);
+            sq[slot] = R::ld(Q + (int64_t)(ok ? v : 0) * KP + col);
         }
     };
 
@@ -666,7 +673,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
     // sample in S; the second half's is f further)
     auto process = [&](int j, int64_t pos) {
         const int u = su[j], v = sv[j];
-        T pv = sp[j], qv = sq[j];
+        V pv = sp[j], qv = sq[j];
         bool fwd = false;
 #pragma unroll
         for (int d = 1; d < D; ++d) {
@@ -681,29 +688,41 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
                 qv = pick(hv[h] == v, hq[h], qv);
             }
         }
-        const float pe = (float)pv, qe = (float)qv;
-        // the product is rounded before the sum (the empty asm keeps it from
-        // fusing into the first cross-lane add), as in run_worker
-        float dot = pe * qe;
+        float p[E], q[E];
+        R::widen(pv, p);
+        R::widen(qv, q);
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            dot += p[e] * q[e];
+        // the lane's sum is rounded before the cross-lane sum (the empty asm
+        // keeps it from fusing into the first cross-lane add), as in run_worker
         asm volatile("" : "+v"(dot));
         const float err = sr[j] - half_sum(dot);
-        float p[1], q[1];
         if constexpr (sizeof(T) == 2) {
             const float step = lr * err;
-            p[0] = __builtin_fmaf(-decay_p, pe, __builtin_fmaf(step, qe, pe));
-            q[0] = __builtin_fmaf(-decay_q, qe, __builtin_fmaf(step, pe, qe));
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float pe = p[e], qe = q[e];
+                p[e] = __builtin_fmaf(-decay_p, pe, __builtin_fmaf(step, qe, pe));
+                q[e] = __builtin_fmaf(-decay_q, qe, __builtin_fmaf(step, pe, qe));
+            }
         } else {
-            p[0] = pe + lr * (err * qe - lp * pe);
-            q[0] = qe + lr * (err * pe - lq * qe);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float pe = p[e], qe = q[e];
+                p[e] = pe + lr * (err * qe - lp * pe);
+                q[e] = qe + lr * (err * pe - lq * qe);
+            }
         }
-        const T np = Row<T, 1>::narrow(p), nq = Row<T, 1>::narrow(q);
+        const V np = R::narrow(p), nq = R::narrow(q);
         if (u >= 0) {
             if constexpr (BUF) {
-                bp.template st<T>(np, cb + (uint32_t)u * kRowBytes, 0);
-                bq.template st<T>(nq, cb + (uint32_t)v * kRowBytes, 0);
+                bp.template st<V>(np, cb + (uint32_t)u * kRowBytes, 0);
+                bq.template st<V>(nq, cb + (uint32_t)v * kRowBytes, 0);
             } else {
-                P[(int64_t)u * KP + col] = np;
-                Q[(int64_t)v * KP + col] = nq;
+                R::st(P + (int64_t)u * KP + col, np);
+                R::st(Q + (int64_t)v * KP + col, nq);
             }
         }
         hu[j] = u;
@@ -711,7 +730,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
         hp[j] = np;
         hq[j] = nq;
         if constexpr (DBG) {
-            if (dbg.visits && col == 0 && u >= 0) {
+            if (dbg.visits && hl == 0 && u >= 0) {
                 const int64_t at = pos + (hi ? f : 0);
                 atomicAdd(dbg.visits + (dbg.orig ? dbg.orig[at] : at), 1u);
             }
@@ -730,7 +749,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
                      int b1) -> bool {
         const int64_t cbase = c_batch * (int64_t)f + c_off;
         if constexpr (DBG) {
-            if (dbg.trace && c_off == 0 && col == 0 && (hi ? a1 : a0) > 0)
+            if (dbg.trace && c_off == 0 && hl == 0 && (hi ? a1 : a0) > 0)
                 dbg.trace[c_batch + (hi ? 1 : 0)] = (int32_t)(w0 + (hi ? 1 : 0));
         }
         if (sync.every > 0 && c_off == 0 && ++batches % sync.every == 0) {

@@ -28,9 +28,13 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
     run_worker<KP, T, D, DBG, false, BUF>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
 }
 
-// The same with rows of 32 values: two workers per wavefront (run_worker_half),
-// wavefront h of the grid being workers 2 h and 2 h + 1.
-template <typename T, int D, bool DBG, bool BUF = false>
+// Row widths whose half-wavefront layout holds at most 16 bytes per lane.
+template <int KP, typename T>
+constexpr bool kHalfRows = sizeof(T) * KP <= 16 * 32;
+
+// The same with two workers per wavefront (run_worker_half), wavefront h of
+// the grid being workers 2 h and 2 h + 1.
+template <int KP, typename T, int D, bool DBG, bool BUF = false>
 __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __restrict__ S, int64_t nnz, int64_t W,
                                                                 int f, T* __restrict__ P, T* __restrict__ Q, float lr,
                                                                 float lp, float lq, DebugSink dbg, int sync_every,
@@ -40,7 +44,7 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
     if (2 * wave >= W)
         return;
     const CacheSync sync{sync_every, (int)blockIdx.x < nx && (threadIdx.x >> 6) == 0, sync_l1 != 0};
-    run_worker_half<T, D, DBG, BUF>(S, nnz, W, wave, f, P, Q, lr, lp, lq, dbg, sync);
+    run_worker_half<KP, T, D, DBG, BUF>(S, nnz, W, wave, f, P, Q, lr, lp, lq, dbg, sync);
 }
 
 // Block-scheduled epoch: wavefront-update (section 3.2.3), and
@@ -220,7 +224,7 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
         if (blk.orig)
             blk.orig += b0;
         if constexpr (HALF)
-            run_worker_half<T, D, DBG>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk);
+            run_worker_half<KP, T, D, DBG>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk);
         else
             run_worker<KP, T, D, DBG, SKIP>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk, CacheSync{0, false, false},
                                             my_sink);
@@ -540,19 +544,20 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
     T* Q = (T*)a.Q;
     if (a.scheme == kSchemeHogwild) {
         const DebugSink dbg{a.visits, nullptr, a.trace_batch};
-        if constexpr (KP == 32) {
+        if constexpr (kHalfRows<KP, T>) {
             if (a.half) {
                 const int64_t blocks = ((a.W + 1) / 2 + 3) / 4;
-                if constexpr (sizeof(T) == 4 && !DBG) {
+                if constexpr (sizeof(T) * KP == 4 * 32 && !DBG) { // one dword of a row per lane
                     if (a.buf) {
-                        hipLaunchKernelGGL((k_hogwild_half<T, D, false, true>), dim3((unsigned)blocks),
+                        hipLaunchKernelGGL((k_hogwild_half<KP, T, D, false, true>), dim3((unsigned)blocks),
                                            dim3(kHogwildBlock), 0, st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq,
                                            dbg, a.sync_every, a.sync_l1, a.nx);
                         return hipGetLastError();
                     }
                 }
-                hipLaunchKernelGGL((k_hogwild_half<T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st,
-                                   a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
+                hipLaunchKernelGGL((k_hogwild_half<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0,
+                                   st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1,
+                                   a.nx);
                 return hipGetLastError();
             }
         }
@@ -655,9 +660,10 @@ static int occupancy_t(bool half)
 {
     int blocks = 0;
     hipError_t e;
-    if constexpr (KP == 32) {
+    if constexpr (kHalfRows<KP, T>) {
         if (half)
-            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild_half<T, D, false>, kHogwildBlock, 0);
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild_half<KP, T, D, false>, kHogwildBlock,
+                                                             0);
         else
             e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_hogwild<KP, T, D, false>, kHogwildBlock, 0);
     } else {

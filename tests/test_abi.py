@@ -64,7 +64,7 @@ def test_options_without_gpu(libpath):
     assert lib.mfsgd_get_option(b"table_workers", ctypes.byref(v)) == 0 and v.value == 0
     assert lib.mfsgd_set_option(b"table_workers", -1) == -1
     assert lib.mfsgd_get_option(b"half_waves", ctypes.byref(v)) == 0 and v.value == 1
-    assert lib.mfsgd_set_option(b"half_waves", 2) == -1
+    assert lib.mfsgd_set_option(b"half_waves", 3) == -1
     assert lib.mfsgd_get_option(b"table_blocks", ctypes.byref(v)) == -4  # read-only, needs init
     lib.mfsgd_get_epoch.restype = ctypes.c_int64
     assert lib.mfsgd_get_epoch() == -1  # not initialised

@@ -281,3 +281,69 @@ def test_block_scheduled_pairs_coverage_and_handover(M, gen, scheme, s, opts):
         for c in range(s):
             prev, nxt = team_of[c, :-1], team_of[c, 1:]
             assert np.all(st[nxt, np.arange(1, s), 0] > st[prev, np.arange(s - 1), 1]), c
+
+
+# ---------------------------------------------------------------------------- wider rows (half_waves = 2)
+@pytest.mark.parametrize("depth", [1, 2, 8])
+@pytest.mark.parametrize("dtype,k", [(np.float32, 50), (np.float32, 128), (np.float16, 64), (np.float16, 128),
+                                     (np.float16, 256)])
+def test_wide_rows_lone_worker_equals_serial(M, depth, dtype, k):
+    """half_waves = 2: two workers per wavefront at wider rows (KP/32 values
+    per lane); one worker equals the serial oracle within the storage
+    tolerance (its lane sums run in another order than one worker per
+    wavefront, so bits may differ)."""
+    rng = np.random.default_rng(7 * depth + k)
+    for m, n, nnz in ((7, 5, 2001), (400, 300, 6037)):
+        S = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+        S["u"] = rng.integers(0, m, nnz)
+        S["v"] = rng.integers(0, n, nnz)
+        S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+        seed = 11 + k
+        P, Q = run(M, S, m, n, k, seed, dtype, workers=1, depth=depth, half_waves=2)
+        Po, Qo = serial(S, m, n, k, seed, dtype)
+        assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype], (m, n)
+
+
+@pytest.mark.parametrize("dtype,k", [(np.float32, 128), (np.float16, 128), (np.float16, 256)])
+@pytest.mark.parametrize("W,f,nnz", [(2, 64, 37 * 64 + 45), (3, 256, 11 * 256 + 200), (8, 64, 8 * 64 * 3 + 64 + 31)])
+def test_wide_rows_disjoint_workers_equal_serial(M, dtype, k, W, f, nnz):
+    rng = np.random.default_rng(W * 31 + k)
+    S, m, n = grouped_samples(rng, W, f, nnz, 6, 4)
+    seed = 5 + W
+    for depth in (1, 2):
+        P, Q = run(M, S, m, n, k, seed, dtype, epochs=2, workers=W, batch_f=f, depth=depth, half_waves=2)
+        Po, Qo = serial(S, m, n, k, seed, dtype, epochs=2)
+        assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype], depth
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_wide_rows_schedule_and_coverage(M, dtype):
+    rng = np.random.default_rng(dtype)
+    m, n, nnz, seed, f = 3000, 2000, 300_017, 9, 256
+    S = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    S["u"] = rng.integers(0, m, nnz)
+    S["v"] = rng.integers(0, n, nnz)
+    S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+    for W in (7, 0):
+        for key, val in dict(DEFAULTS, dtype=dtype, debug=3, workers=W, half_waves=2).items():
+            M.set_option(key, val)
+        M.init(m, n, 128, seed)
+        M.epoch(M.samples_to_device(S), 0.001, 0.05, 0.05, "hogwild")
+        assert np.all(M.debug_visits(nnz).cpu().numpy() == 1)
+        nb = (nnz + f - 1) // f
+        Wd = W if W else min(2 * M.get_option("resident_waves"), nb)
+        assert np.array_equal(M.debug_trace(nb).cpu().numpy(), oracle.hogwild_batch_owner(nnz, f, Wd))
+
+
+def test_half_workers_choice(M):
+    """Read-only key half_workers: two workers per wavefront at k <= 32 by
+    default; at every width of at most 16 bytes per lane with half_waves = 2;
+    never with 0."""
+    cases = [(1, 0, 32, 1), (1, 1, 32, 1), (1, 0, 64, 0), (1, 0, 128, 0), (1, 1, 64, 0), (1, 1, 128, 0),
+             (1, 1, 256, 0), (2, 0, 128, 1), (2, 0, 256, 0), (2, 1, 256, 1), (2, 1, 512, 0), (0, 0, 32, 0),
+             (0, 1, 128, 0)]
+    for half, dtype, k, want in cases:
+        for key, val in dict(DEFAULTS, dtype=dtype, half_waves=half).items():
+            M.set_option(key, val)
+        M.init(50, 40, k, 1)
+        assert M.get_option("half_workers") == want, (half, dtype, k)
