@@ -137,7 +137,7 @@ struct Context {
     const Plan* lay_plan = nullptr;
     uint64_t lay_version = 0;
     int64_t lay_want = -1;
-    int lay_grid = 0, lay_waves = 0, lay_depth = 0;
+    int lay_grid = 0, lay_waves = 0, lay_depth = 0, lay_half = -1;
 };
 
 Options g_opt;
@@ -309,10 +309,10 @@ int occupancy_waves(int KP, int dtype, int depth)
     return dtype == MFSGD_FP16 ? occupancy_f16(KP, depth, half) : occupancy_f32(KP, depth, half);
 }
 
-int occupancy_blocked(int KP, int dtype, int depth, int threads)
+int occupancy_blocked(int KP, int dtype, int depth, int threads, bool half = false)
 {
-    return dtype == MFSGD_FP16 ? occupancy_blocked_f16(KP, depth, threads)
-                               : occupancy_blocked_f32(KP, depth, threads);
+    return dtype == MFSGD_FP16 ? occupancy_blocked_f16(KP, depth, threads, half ? 1 : 0)
+                               : occupancy_blocked_f32(KP, depth, threads, half ? 1 : 0);
 }
 
 // Read back and clear the device error flag; the stream has been synchronised.
@@ -959,14 +959,14 @@ bool skip_stores(const Plan& pl)
 // team; 0: every workgroup slot the occupancy allows, home teams shared in
 // proportion to the row blocks' samples, every wavefront also serving the
 // other teams of its XCD).
-int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
+int team_layout(const Plan& pl, int64_t want, bool half, EpochLaunch& a)
 {
     Context& c = g;
     const int s = pl.s;
     const int waves = want == 1 ? 1 : 4;
     const int nx = std::max(1, c.nx);
     if (c.lay_plan != &pl || c.lay_version != pl.version || c.lay_want != want || c.lay_waves != waves ||
-        c.lay_depth != a.depth) {
+        c.lay_depth != a.depth || c.lay_half != (int)half) {
         TeamLayout L;
         if (want == 1) {
             L.grid = s;
@@ -976,7 +976,7 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
                 L.tmap[t] = t << 16;
             L.xteams.assign((size_t)nx * (kMaxGrid + 1), 0);
         } else {
-            const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 64 * waves);
+            const int per_cu = occupancy_blocked(c.KP, c.dtype, a.depth, 64 * waves, half);
             if (per_cu <= 0)
                 return fail(MFSGD_EHIP, "occupancy query failed for the block-scheduled kernel");
             // Work is claimed, not assigned, so no workgroup has to be
@@ -1003,6 +1003,7 @@ int team_layout(const Plan& pl, int64_t want, EpochLaunch& a)
         c.lay_want = want;
         c.lay_waves = waves;
         c.lay_depth = a.depth;
+        c.lay_half = (int)half;
         c.lay_grid = (int)L.grid;
     }
     a.grid = c.lay_grid;
@@ -1111,8 +1112,9 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.S = pl->Sp;
         a.bstart = pl->bstart;
         a.s = s;
-        CHK(team_layout(*pl, want, a));
-        if (hog && want != 1 && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1) {
+        const bool pairs = hog && want != 1 && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1;
+        CHK(team_layout(*pl, want, pairs, a));
+        if (pairs) {
             // Partitioned batch-Hogwild! at k <= 32: pooled wavefronts claim
             // two batches at a time and run one per half, in place of skipped
             // stores (measured faster on the Netflix shape at k = 32; pairs

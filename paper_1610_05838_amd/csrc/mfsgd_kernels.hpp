@@ -441,9 +441,16 @@ __global__ __launch_bounds__(64) void k_wave(const Sample* __restrict__ Sp, cons
 }
 
 template <int KP, typename T, int D>
-static int occupancy_blocked_t(int threads)
+static int occupancy_blocked_t(int threads, bool half)
 {
     int blocks = 0;
+    if constexpr (KP == 32) {
+        if (half) // the only variant such launches use
+            return hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false, false, true>,
+                                                                threads, 0) == hipSuccess
+                       ? blocks
+                       : 0;
+    }
     // the co-residency cap must hold for both variants the launcher may pick
     int plain = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false, true>, threads, 0) !=
@@ -451,24 +458,17 @@ static int occupancy_blocked_t(int threads)
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&plain, k_blocked<KP, T, D, false, false>, threads, 0) !=
             hipSuccess)
         return 0;
-    if constexpr (KP == 32) {
-        int half = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&half, k_blocked<KP, T, D, false, false, true>, threads, 0) !=
-            hipSuccess)
-            return 0;
-        plain = half < plain ? half : plain;
-    }
     return blocks < plain ? blocks : plain;
 }
 
 template <int KP, typename T>
-static int occupancy_blocked_kp(int depth, int threads)
+static int occupancy_blocked_kp(int depth, int threads, bool half)
 {
     switch (depth) {
-    case 1: return occupancy_blocked_t<KP, T, 1>(threads);
-    case 2: return occupancy_blocked_t<KP, T, 2>(threads);
-    case 4: return occupancy_blocked_t<KP, T, 4>(threads);
-    case 8: return occupancy_blocked_t<KP, T, 8>(threads);
+    case 1: return occupancy_blocked_t<KP, T, 1>(threads, half);
+    case 2: return occupancy_blocked_t<KP, T, 2>(threads, half);
+    case 4: return occupancy_blocked_t<KP, T, 4>(threads, half);
+    case 8: return occupancy_blocked_t<KP, T, 8>(threads, half);
     default: return 0;
     }
 }
@@ -737,14 +737,14 @@ struct Dispatch {
         default: return 0;
         }
     }
-    static int occupancy_blocked(int KP, int depth, int threads)
+    static int occupancy_blocked(int KP, int depth, int threads, bool half)
     {
         switch (KP) {
-        case 32: return occupancy_blocked_kp<32, T>(depth, threads);
-        case 64: return occupancy_blocked_kp<64, T>(depth, threads);
-        case 128: return occupancy_blocked_kp<128, T>(depth, threads);
-        case 256: return occupancy_blocked_kp<256, T>(depth, threads);
-        case 512: return occupancy_blocked_kp<512, T>(depth, threads);
+        case 32: return occupancy_blocked_kp<32, T>(depth, threads, half);
+        case 64: return occupancy_blocked_kp<64, T>(depth, threads, false);
+        case 128: return occupancy_blocked_kp<128, T>(depth, threads, false);
+        case 256: return occupancy_blocked_kp<256, T>(depth, threads, false);
+        case 512: return occupancy_blocked_kp<512, T>(depth, threads, false);
         default: return 0;
         }
     }

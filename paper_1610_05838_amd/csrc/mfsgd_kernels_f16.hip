@@ -9,9 +9,9 @@ hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st) { return Dispat
 
 int occupancy_f16(int KP, int depth, int half) { return Dispatch<half_t>::occupancy(KP, depth, half != 0); }
 
-int occupancy_blocked_f16(int KP, int depth, int threads)
+int occupancy_blocked_f16(int KP, int depth, int threads, int half)
 {
-    return Dispatch<half_t>::occupancy_blocked(KP, depth, threads);
+    return Dispatch<half_t>::occupancy_blocked(KP, depth, threads, half != 0);
 }
 
 hipError_t rmse_partial_f16(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,

@@ -96,8 +96,9 @@ hipError_t table_epoch_f16(const TableLaunch& a, hipStream_t st);
 // wavefronts of the one-address-space batch-Hogwild! kernel per CU (half: two workers per wavefront)
 int occupancy_f32(int KP, int depth, int half);
 int occupancy_f16(int KP, int depth, int half);
-int occupancy_blocked_f32(int KP, int depth, int threads); // workgroups per CU
-int occupancy_blocked_f16(int KP, int depth, int threads);
+// workgroups per CU (half: the launch runs two batches per claim)
+int occupancy_blocked_f32(int KP, int depth, int threads, int half);
+int occupancy_blocked_f16(int KP, int depth, int threads, int half);
 hipError_t rmse_partial_f32(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
                             hipStream_t st);
 hipError_t rmse_partial_f16(int KP, const Sample* S, int64_t ntest, const void* P, const void* Q, double* partial,
