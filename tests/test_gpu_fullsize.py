@@ -126,3 +126,38 @@ def test_deterministic_wavefront_at_full_size_matches_oracle(M, netflix):
     print(f"full-size deterministic wavefront: max-abs P {np.abs(P - Po).max():.3g} Q {np.abs(Q - Qo).max():.3g}")
     assert float(np.abs(P - Po).max()) <= 1e-4 and float(np.abs(Q - Qo).max()) <= 1e-4
     assert M.rmse(dT) == pytest.approx(oracle.rmse(Po, Qo, T), rel=1e-5)
+
+
+def test_half_wavefront_workers_at_full_size(M, netflix):
+    """The Netflix shape trained at k = 32 (same samples): one address space
+    with two workers per wavefront (every resident slot: 2 x resident
+    wavefronts) uses every sample once with batch b on worker b mod W and
+    trains; the automatic (partitioned) form with paired claims uses every
+    sample once in the oracle's column orders."""
+    import torch
+    w, S, T, dS, dT = netflix
+    f = 256
+    nb = (len(S) + f - 1) // f
+    reset(M, partition=0, debug=3)
+    M.init(w["m"], w["n"], 32, w["seed"])
+    assert M.get_option("half_workers") == 1
+    r0 = M.rmse(dT)
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    assert bool(torch.all(M.debug_visits(len(S)) == 1))
+    W = min(2 * M.get_option("resident_waves"), nb)
+    assert np.array_equal(M.debug_trace(nb).cpu().numpy(), oracle.hogwild_batch_owner(len(S), f, W))
+    M.set_option("debug", 0)
+    hist = [r0, M.rmse(dT)]
+    for t in range(1, 3):
+        M.epoch(dS, w["lr"] * w["decay"] ** t, w["lam"], w["lam"], "hogwild")
+        hist.append(M.rmse(dT))
+    print("k = 32 half-wavefront test rmse by epoch", hist)
+    assert all(b < a for a, b in zip(hist, hist[1:]))
+    reset(M, debug=3)
+    M.init(w["m"], w["n"], 32, w["seed"])
+    assert M.get_option("partitioned") == 1  # 63.7 MB of factors
+    x = M.get_option("xcds")
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    assert bool(torch.all(M.debug_visits(len(S)) == 1))
+    tr = M.debug_trace(3 * x * x).cpu().numpy()
+    assert np.array_equal(tr[:x * x].reshape(x, x), oracle.wavefront_sigma(w["seed"], 0, x))
