@@ -255,6 +255,19 @@ def block_order(S, m, n, s, balanced=False):
     return order[:len(S)], start
 
 
+def block_starts(S, m, n, s, balanced=False) -> np.ndarray:
+    """start[b] = first position of block b in the stable bucketing (the
+    `start` of block_order, without the order array)."""
+    S = _samples(S)
+    start = np.empty(s * s + 1, dtype=np.int64)
+    rb = balanced_bounds(S, m, 0, s) if balanced else None
+    cb = balanced_bounds(S, n, 1, s) if balanced else None
+    if lib().orc_block_order(_ptr(S), len(S), m, n, s, None if rb is None else _ptr(rb),
+                             None if cb is None else _ptr(cb), None, _ptr(start)):
+        raise MemoryError
+    return start
+
+
 def rmse(P, Qt, T) -> float:
     T = _samples(T)
     return lib().orc_rmse(P.shape[1], _dtype_code(P), _ptr(P), _ptr(Qt), _ptr(T), len(T))

@@ -380,7 +380,7 @@ int orc_block_order(const orc_sample* S, int64_t nnz, int64_t m, int64_t n, int3
         start[orc_block_id(&S[i], m, n, s, rb, cb) + 1]++;
     for (int64_t b = 0; b < nb; b++)
         start[b + 1] += start[b];
-    for (int64_t i = 0; i < nnz; i++) {
+    for (int64_t i = 0; order && i < nnz; i++) { /* order == NULL: block starts only */
         int64_t b = orc_block_id(&S[i], m, n, s, rb, cb);
         order[start[b] + fill[b]++] = i;
     }

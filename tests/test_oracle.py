@@ -518,3 +518,106 @@ def test_table_lr_zero_is_identity(orc):
     P1, Q1 = P.copy(), Q.copy()
     orc.epoch_table(P1, Q1, S, 0.0, 0.05, 0.05, 4, 2, 0)
     assert np.array_equal(P1, P) and np.array_equal(Q1, Q)
+
+
+# ---------------------------------------------------------------------------- section 2.2 objective
+def test_objective_hand_example(orc):
+    g = gold("objective_hand.json")
+    P = np.array(g["P"], dtype=np.float32)
+    Q = np.array(g["Qt"], dtype=np.float32)
+    S = samples(g["samples"], orc)
+    assert orc.objective(P, Q, S, g["lambda_p"], g["lambda_q"]) == g["objective"]
+    # one term per sample
+    for row, term in zip(g["samples"], g["terms"]):
+        assert orc.objective(P, Q, samples([row], orc), g["lambda_p"], g["lambda_q"]) == term
+
+
+def test_objective_without_regularisation_is_sum_of_squared_errors(orc):
+    """With lambda = 0 the cost is N * RMSE^2 over the same samples (ties the
+    objective to the RMSE routine, written separately)."""
+    rng = np.random.default_rng(11)
+    m, n, k, N = 40, 30, 8, 500
+    P = rng.normal(size=(m, k)).astype(np.float32)
+    Q = rng.normal(size=(n, k)).astype(np.float32)
+    S = np.zeros(N, dtype=orc.SAMPLE_DTYPE)
+    S["u"], S["v"], S["r"] = rng.integers(0, m, N), rng.integers(0, n, N), rng.normal(size=N)
+    obj = orc.objective(P, Q, S, 0.0, 0.0)
+    assert obj == pytest.approx(N * orc.rmse(P, Q, S) ** 2, rel=1e-12)
+    # the regularisers add lambda |row|^2 once per sample that uses the row
+    lp, lq = 0.3, 0.7
+    reg = sum(lp * float(np.dot(P[u].astype(np.float64), P[u])) + lq * float(np.dot(Q[v].astype(np.float64), Q[v]))
+              for u, v in zip(S["u"], S["v"]))
+    assert orc.objective(P, Q, S, lp, lq) == pytest.approx(obj + reg, rel=1e-12)
+
+
+def test_update_descends_the_objective(orc):
+    """A single-sample epoch moves (p, q) along minus half the gradient of that
+    sample's cost, so for a small rate the objective drops by lr/2 times the
+    squared gradient norm, up to a second-order term of relative size ~lr."""
+    rng = np.random.default_rng(5)
+    k = 8
+    P = rng.normal(size=(1, k)).astype(np.float32)
+    Q = rng.normal(size=(1, k)).astype(np.float32)
+    r, lp, lq, lr = 0.9, 0.2, 0.4, 1e-3
+    S = samples([(0, 0, r)], orc)
+    p, q = P[0].astype(np.float64), Q[0].astype(np.float64)
+    e = r - p @ q
+    gp = -2 * e * q + 2 * lp * p
+    gq = -2 * e * p + 2 * lq * q
+    f0 = orc.objective(P, Q, S, lp, lq)
+    orc.epoch_serial(P, Q, S, lr, lp, lq)
+    f1 = orc.objective(P, Q, S, lp, lq)
+    assert f0 - f1 == pytest.approx(0.5 * lr * (gp @ gp + gq @ gq), rel=2e-2)
+
+
+# ---------------------------------------------------------------------------- OpenMP Hogwild! timing variant
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_openmp_hogwild_one_thread_is_serial(orc, dtype):
+    """With one thread the batches are claimed in order, so the timing variant
+    is the serial epoch bit for bit (ragged last batch included)."""
+    rng = np.random.default_rng(3)
+    m, n, k, N, f = 60, 45, 16, 3 * 256 + 77, 256
+    P0, Q0 = orc.init_factors(m, n, k, 99, dtype)
+    S = np.zeros(N, dtype=orc.SAMPLE_DTYPE)
+    S["u"], S["v"], S["r"] = rng.integers(0, m, N), rng.integers(0, n, N), rng.normal(size=N)
+    Pa, Qa, Pb, Qb = P0.copy(), Q0.copy(), P0.copy(), Q0.copy()
+    orc.epoch_serial(Pa, Qa, S, 0.05, 0.02, 0.03)
+    used = orc.epoch_hogwild_omp(Pb, Qb, S, 0.05, 0.02, 0.03, f=f, nthreads=1)
+    assert used == 1
+    assert np.array_equal(Pa.view(np.uint8), Pb.view(np.uint8)) and np.array_equal(Qa.view(np.uint8), Qb.view(np.uint8))
+
+
+@pytest.mark.parametrize("f", [16, 64])
+def test_openmp_hogwild_disjoint_batches_equal_serial(orc, f):
+    """Several threads on batches whose rows are disjoint: every batch commutes
+    with every other, so the result is the serial epoch bit for bit whatever
+    the interleaving.  A batch run twice, a sample skipped or a batch bound
+    off by one would change some row."""
+    rng = np.random.default_rng(17)
+    nb, k, ru, rv = 97, 8, 3, 2          # rows per batch: ru users, rv items
+    N = nb * f - f // 2                  # ragged last batch
+    m, n = nb * ru, nb * rv
+    S = np.zeros(N, dtype=orc.SAMPLE_DTYPE)
+    b = np.arange(N) // f
+    S["u"] = b * ru + rng.integers(0, ru, N)
+    S["v"] = b * rv + rng.integers(0, rv, N)
+    S["r"] = rng.normal(size=N)
+    P0, Q0 = orc.init_factors(m, n, k, 5, np.float32)
+    Pa, Qa, Pb, Qb = P0.copy(), Q0.copy(), P0.copy(), Q0.copy()
+    orc.epoch_serial(Pa, Qa, S, 0.1, 0.05, 0.05)
+    used = orc.epoch_hogwild_omp(Pb, Qb, S, 0.1, 0.05, 0.05, f=f, nthreads=4)
+    assert used == 4
+    assert np.array_equal(Pa, Pb) and np.array_equal(Qa, Qb)
+    # every row moved (no batch was skipped)
+    assert (Pb != P0).any(axis=1).all() and (Qb != Q0).any(axis=1).all()
+
+
+@pytest.mark.parametrize("balanced", [False, True])
+def test_block_starts_equal_block_order_starts(orc, balanced):
+    rng = np.random.default_rng(23)
+    m, n, N, s = 300, 170, 20_000, 7
+    S = np.zeros(N, dtype=orc.SAMPLE_DTYPE)
+    S["u"] = (rng.zipf(1.6, N) - 1) % m
+    S["v"] = rng.integers(0, n, N)
+    order, start = orc.block_order(S, m, n, s, balanced=balanced)
+    assert np.array_equal(orc.block_starts(S, m, n, s, balanced=balanced), start)
