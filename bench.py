@@ -1,17 +1,26 @@
-"""Benchmark: SGD updates/s and achieved HBM bandwidth of the batch-Hogwild!
-epoch at k=128 on one MI355X.
+"""Benchmark: SGD updates/s and achieved HBM GB/s of the SGD-MF epoch at k=128
+on one MI355X.
 
-Workload (default): the Netflix-shaped synthetic set -- m=480,189 users,
-n=17,770 items, 99,072,112 training ratings (+1,408,395 test), Zipf(1.0)
-user and item popularity, k=128, binary32 feature storage, lr 0.003 x 0.99^t,
-lambda 0.05, batch-Hogwild! with f=256.  A step is one full epoch (every
-training rating updates P and Q once) followed by the test RMSE, with all
-inputs resident in HBM.
+Headline workload (default): the Hugewiki-shaped synthetic set, the largest
+of the paper's data sets that one GPU holds -- m=50,082,603 users, n=39,780
+items, 3,069,000,000 training ratings (+31,000,000 test, 36.8 GB of samples),
+Zipf(1.0) users, uniform items, k=128, binary16 feature storage (12.8 GB of
+P), lr 0.01, lambda 0.01, wavefront-update on a 64 x 64 grid (the paper's
+schedule for it).  A step is one full epoch (every training rating updates P
+and Q once) followed by the test RMSE, with all inputs resident in HBM; the
+wavefront plan is made once before the timed steps.
 
-Printed: one JSON line (rank 0) with the whole-run updates/s, the roofline of
-the epoch kernel (algorithmic bytes per update 4k*sizeof(feature)+12 over the
-kernel's HIP-event time, against 8 TB/s) and the CPU oracle timed on a bounded
-prefix of the same workload.
+Two more lines ride along in the same JSON object ("extra"): the
+Netflix-shaped set (binary32, the default batch-Hogwild!) and the
+Yahoo!Music-shaped set (binary32, 832 MB of factors, the default
+batch-Hogwild!), each with its own epoch time, updates/s, algorithmic
+bandwidth and test RMSE (--no-extra skips them).
+
+Printed: one JSON line with the whole-run updates/s, the roofline of the
+epoch kernel (algorithmic bytes per update 4k*sizeof(feature)+12 over the
+kernel's HIP-event time, against 8 TB/s; measured HBM traffic from the
+committed rocprofv3 counter summary when it was taken on the current
+sources) and the CPU oracle timed on a bounded prefix of the same workload.
 """
 from __future__ import annotations
 
@@ -80,6 +89,11 @@ def cpu_baseline(w, S, target_s: float, threads: int):
     """The oracle (never tuned) on a bounded prefix of the same workload.
     S: a host prefix of the training samples, long enough for target_s."""
     import numpy as np
+
+    # the OpenMP runtime the oracle loads reads these once: one thread per
+    # physical core, spread over the sockets
+    os.environ["OMP_PROC_BIND"] = "spread"
+    os.environ["OMP_PLACES"] = "cores"
     import oracle
 
     dtype = np.float16 if w["dtype"] == "fp16" else np.float32
@@ -182,28 +196,195 @@ def shard_share(args):
         flush=True)
 
 
+def oracle_threads():
+    """Threads for the OpenMP oracle: the physical cores (lscpu's core ids)
+    among the CPUs this process may run on, capped by OMP_NUM_THREADS when it
+    is set (the machine's share for this job).  Returns (threads, physical
+    cores seen)."""
+    import subprocess
+
+    cpus = set(os.sched_getaffinity(0))
+    cores = set()
+    try:
+        out = subprocess.run(["lscpu", "-p=CPU,CORE,SOCKET"], capture_output=True, text=True, timeout=30).stdout
+        for line in out.splitlines():
+            if line.startswith("#") or not line.strip():
+                continue
+            cpu, core, sock = line.split(",")[:3]
+            if int(cpu) in cpus:
+                cores.add((sock, core))
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    physical = len(cores) or len(cpus)
+    n = physical
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n), physical
+
+
+def kernel_of(mfsgd, scheme, staged):
+    """Name of the epoch kernel a launch runs."""
+    if scheme == "table":
+        return "k_table"
+    if scheme != "hogwild" or (mfsgd.get_option("partitioned") == 1 and not staged):
+        return "k_blocked"
+    return "k_hogwild_half" if mfsgd.get_option("half_workers") else "k_hogwild"
+
+
+def apply_options(mfsgd, args, dtype):
+    mfsgd.reset_options()
+    mfsgd.set_option("dtype", dtype)
+    for key, val in (("workers", args.workers), ("depth", args.depth), ("team_waves", args.team_waves)):
+        if val:
+            mfsgd.set_option(key, val)
+    if args.partition is not None:
+        mfsgd.set_option("partition", args.partition)
+    for kv in args.set:
+        key, val = kv.split("=", 1)
+        mfsgd.set_option(key, int(val))
+
+
+def measure(args, name, scheme, steps, warmup, dev, host_prefix=0):
+    """Generate the workload into HBM, run `warmup` then `steps` timed steps
+    (epoch + test RMSE) of `scheme`, and return the measurements."""
+    import numpy as np
+    import torch
+
+    from paper_1610_05838_amd import datagen, mfsgd
+
+    w = datagen.workload(name)
+    if args.ntrain:
+        w["ntrain"] = args.ntrain
+    t0 = time.perf_counter()
+    S = None
+    if args.staged:
+        if scheme != "hogwild":
+            raise SystemExit("--staged runs batch-Hogwild! only")
+        S = datagen.draw(w, 0, w["ntrain"]) if w["draw"] == "independent" else datagen.make(w)[0]
+        T = datagen.draw(w, w["ntrain"], w["ntest"]) if w["draw"] == "independent" else datagen.make(w)[1]
+        dS = torch.from_numpy(S.view(np.int32).reshape(-1, 3)).pin_memory()
+    elif w["draw"] == "independent":
+        # generated chunk by chunk straight into HBM; the host keeps a prefix for the CPU baseline
+        dS = datagen.draw_to_device(w, 0, w["ntrain"], dev, chunk=1 << 27, progress=lambda a, b: (
+            log(f"  generated {a}/{b}") if a % (1 << 30) < (1 << 27) else None))
+        T = datagen.draw(w, w["ntrain"], w["ntest"])
+        if host_prefix:
+            S = datagen.draw(w, 0, min(w["ntrain"], host_prefix))
+    else:
+        S, T = datagen.make(w)
+        dS = mfsgd.samples_to_device(S, dev)
+    dT = mfsgd.samples_to_device(T, dev)
+    nnz = w["ntrain"]
+    if args.k:
+        w["k"] = args.k  # after generation: only the trained width changes
+    log(f"generated {w['name']}: {nnz} train + {len(T)} test in {time.perf_counter() - t0:.1f}s")
+    dtype = 1 if w["dtype"] == "fp16" else 0
+    apply_options(mfsgd, args, dtype)
+    mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
+    kernel = kernel_of(mfsgd, scheme, args.staged)
+    grid_s = args.grid_s or w.get("grid_s", 32)
+    if scheme == "table":
+        grid_s = mfsgd.get_option("table_grid")
+        if warmup < 1:
+            raise SystemExit("--scheme table plans in its first epoch: use --warmup 1 or more")
+    elif scheme != "hogwild":
+        t0 = time.perf_counter()
+        mfsgd.plan(dS, grid_s)
+        log(f"wavefront plan (s={grid_s}) {time.perf_counter() - t0:.3f}s")
+    stream = torch.cuda.current_stream()
+
+    def step(t, ev=None):
+        lr = datagen.lr_at(w, t)
+        if ev is not None:
+            ev[0].record(stream)
+        if args.staged:
+            mfsgd.epoch_staged(dS, lr, w["lam"], w["lam"], stream)
+        else:
+            mfsgd.epoch(dS, lr, w["lam"], w["lam"], scheme, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        return mfsgd.rmse(dT, stream)
+
+    rmses = []
+    for t in range(warmup):
+        rmses.append(step(t))
+        log(f"{name} warmup epoch {t}: test rmse {rmses[-1]:.5f}")
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        rmses.append(step(warmup + i, events[i]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    epoch_ms = [a.elapsed_time(b) for a, b in events]
+    log(f"{name}: timed {steps} steps in {wall:.3f}s; epoch kernel ms: " + ", ".join(f"{x:.2f}" for x in epoch_ms))
+    log(f"{name}: test rmse after each epoch: " + ", ".join(f"{x:.4f}" for x in rmses))
+    r = dict(w=w, scheme=scheme, grid_s=grid_s, nnz=nnz, ntest=len(T), epoch_ms=epoch_ms, rmses=rmses, wall=wall,
+             kernel=kernel, S=S, dtype=dtype, resident=mfsgd.get_option("resident_waves"),
+             partitioned=scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged)
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        for i in range(3):
+            b.copy_(a)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
+        log("copy calibration: 3 x 4 GiB device copies, " + ", ".join(
+            f"{x:.2f} ms ({2 * a.numel() * 4 / x / 1e6:.0f} GB/s read+write)" for x in ms))
+        del a, b
+    mfsgd.finalize()
+    del dS, dT
+    torch.cuda.empty_cache()
+    return r
+
+
+def rates(r):
+    """Epoch-kernel rates of one measurement."""
+    w = r["w"]
+    bpu = 4 * w["k"] * (2 if r["dtype"] else 4) + 12
+    avg_s = sum(r["epoch_ms"]) / len(r["epoch_ms"]) / 1e3
+    gbs = r["nnz"] * bpu / avg_s / 1e9
+    return bpu, avg_s, gbs
+
+
+def describe(r):
+    w = r["w"]
+    return (f"{w['name']}: m={w['m']} n={w['n']} k={w['k']} nnz={r['nnz']} ntest={r['ntest']} {w['dtype']} "
+            f"{r['scheme']}" + (f" s={r['grid_s']}" if r["scheme"] != "hogwild" else " f=256"))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="netflix")
-    ap.add_argument("--scheme", default="hogwild", choices=["hogwild", "wavefront", "wavefront_det", "table"],
-                    help="table: the global scheduling table (LIBMF's policy; --set table_grid=S --set "
+    ap.add_argument("--workload", default="hugewiki")
+    ap.add_argument("--scheme", default="", choices=["", "hogwild", "wavefront", "wavefront_det", "table"],
+                    help="default: wavefront-update for workloads that name a grid (hugewiki), else batch-Hogwild!; "
+                         "table: the global scheduling table (LIBMF's policy; --set table_grid=S --set "
                          "table_workers=W), planned in the first warm-up epoch")
     ap.add_argument("--grid-s", type=int, default=0, help="wavefront grid side (0: the workload's, else 32)")
     ap.add_argument("--workers", type=int, default=0)
-    ap.add_argument("--depth", type=int, default=2)
+    ap.add_argument("--depth", type=int, default=0, help="samples in flight per wavefront (0: the library's choice)")
     ap.add_argument("--team-waves", type=int, default=0)
-    ap.add_argument("--partition", type=int, default=2, help="batch-Hogwild!: 0 one address space, 1 XCD-partitioned, 2 automatic")
+    ap.add_argument("--partition", type=int, default=None,
+                    help="batch-Hogwild! form: 0 one address space, 1 XCD-partitioned, 2 one XCD (library default), "
+                         "3 partitioned without tickets")
     ap.add_argument("--ntrain", type=int, default=0, help="override the training size (0: the workload's)")
     ap.add_argument("--k", type=int, default=0,
                     help="train at this width instead of the workload's (same samples; 0: the workload's k)")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
                     help="further library option (mfsgd_set_option), applied before init")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--cpu-threads", type=int, default=16)
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="OpenMP oracle threads (0: the physical cores available, capped by OMP_NUM_THREADS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the Netflix- and Yahoo-shaped extra lines")
+    ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--staged", action="store_true",
                     help="training samples stay in pinned host memory and stream through the GPU (mfsgd_epoch_staged, "
                          "batch-Hogwild!): value then includes the PCIe transfers and is not the resident rate")
@@ -226,122 +407,35 @@ def main():
         shard_share(args)
         return
 
-    import numpy as np
     import torch
-
-    from paper_1610_05838_amd import datagen, mfsgd
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = datagen.workload(args.workload)
-    if args.ntrain:
-        w["ntrain"] = args.ntrain
-    t0 = time.perf_counter()
-    if args.staged:
-        if args.scheme != "hogwild":
-            raise SystemExit("--staged runs batch-Hogwild! only")
-        S = datagen.draw(w, 0, w["ntrain"]) if w["draw"] == "independent" else datagen.make(w)[0]
-        T = datagen.draw(w, w["ntrain"], w["ntest"]) if w["draw"] == "independent" else datagen.make(w)[1]
-        dS = torch.from_numpy(S.view(np.int32).reshape(-1, 3)).pin_memory()
-    elif w["draw"] == "independent":
-        # generated chunk by chunk straight into HBM; the host keeps a prefix for the CPU baseline
-        dS = datagen.draw_to_device(w, 0, w["ntrain"], dev, progress=lambda a, b: (
-            log(f"  generated {a}/{b}") if a % (1 << 29) < (1 << 25) else None))
-        T = datagen.draw(w, w["ntrain"], w["ntest"])
-        S = datagen.draw(w, 0, min(w["ntrain"], 50_000_000 if args.cpu_threads > 1 else 20_000_000))
-    else:
-        S, T = datagen.make(w)
-        dS = mfsgd.samples_to_device(S, dev)
-    dT = mfsgd.samples_to_device(T, dev)
-    nnz = w["ntrain"]
-    if args.k:
-        w["k"] = args.k  # after generation: only the trained width changes
-    log(f"generated {w['name']}: {nnz} train + {len(T)} test in {time.perf_counter() - t0:.1f}s")
-
-    dtype = 1 if w["dtype"] == "fp16" else 0
-    feat_bytes = 2 if dtype else 4
-    for key, val in dict(dtype=dtype, batch_f=256, workers=args.workers, depth=args.depth,
-                         team_waves=args.team_waves, partition=args.partition, debug=0).items():
-        mfsgd.set_option(key, val)
-    for kv in args.set:
-        key, val = kv.split("=", 1)
-        mfsgd.set_option(key, int(val))
-    mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
-    resident = mfsgd.get_option("resident_waves")
-    partitioned = args.scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged
-    kernel = "k_hogwild" if (args.scheme == "hogwild" and not partitioned) else "k_blocked"
-    if kernel == "k_hogwild" and mfsgd.get_option("half_workers"):
-        kernel = "k_hogwild_half"
-    grid_s = args.grid_s or w.get("grid_s", 32)
-    if args.scheme == "table":
-        kernel = "k_table"
-        grid_s = mfsgd.get_option("table_grid")
-        if args.warmup < 1:
-            raise SystemExit("--scheme table plans in its first epoch: use --warmup 1 or more")
-    elif args.scheme != "hogwild":
-        t0 = time.perf_counter()
-        mfsgd.plan(dS, grid_s)
-        log(f"wavefront plan (s={grid_s}) {time.perf_counter() - t0:.3f}s")
-    stream = torch.cuda.current_stream()
-
-    def step(t, ev=None):
-        lr = datagen.lr_at(w, t)
-        if ev is not None:
-            ev[0].record(stream)
-        if args.staged:
-            mfsgd.epoch_staged(dS, lr, w["lam"], w["lam"], stream)
-        else:
-            mfsgd.epoch(dS, lr, w["lam"], w["lam"], args.scheme, stream)
-        if ev is not None:
-            ev[1].record(stream)
-        return mfsgd.rmse(dT, stream)
-
-    rmses = []
-    for t in range(args.warmup):
-        rmses.append(step(t))
-        log(f"warmup epoch {t}: test rmse {rmses[-1]:.5f}")
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        rmses.append(step(args.warmup + i, events[i]))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    epoch_ms = [a.elapsed_time(b) for a, b in events]
-    log(f"timed {args.steps} steps in {wall:.3f}s; epoch kernel ms: " + ", ".join(f"{x:.2f}" for x in epoch_ms))
-    log(f"test rmse after each epoch: " + ", ".join(f"{x:.4f}" for x in rmses))
+    # the paper runs Hugewiki under wavefront-update (its own section 3.2.3 grid), the others under batch-Hogwild!
+    scheme = args.scheme or ("wavefront" if args.workload == "hugewiki" else "hogwild")
+    threads, physical = oracle_threads()
+    if args.cpu_threads:
+        threads = args.cpu_threads
+    r = measure(args, args.workload, scheme, args.steps, args.warmup, dev,
+                host_prefix=0 if args.no_cpu_baseline else (50_000_000 if threads > 1 else 20_000_000))
+    w = r["w"]
     if args.log_jsonl:
-        bpu = 4 * w["k"] * (2 if w["dtype"] == "fp16" else 4) + 12
+        bpu = rates(r)[0]
         with open(args.log_jsonl, "w") as f:
-            for i, ms in enumerate(epoch_ms):
-                ups = nnz / (ms / 1e3)
-                f.write(json.dumps({"workload": w["name"], "scheme": args.scheme, "dtype": w["dtype"],
+            for i, ms in enumerate(r["epoch_ms"]):
+                ups = r["nnz"] / (ms / 1e3)
+                f.write(json.dumps({"workload": w["name"], "scheme": scheme, "dtype": w["dtype"],
                                     "epoch": args.warmup + i + 1, "epoch_ms": ms, "updates_per_s": ups,
                                     "algorithmic_gbs": ups * bpu / 1e9, "frac_of_peak": ups * bpu / 1e9 / HBM_PEAK_GBS,
-                                    "test_rmse": rmses[args.warmup + i]}) + "\n")
-
-    if args.copy_calibration:
-        a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
-        b = torch.empty_like(a)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        ev[0].record(stream)
-        for i in range(3):
-            b.copy_(a)
-            ev[i + 1].record(stream)
-        torch.cuda.synchronize()
-        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
-        log("copy calibration: 3 x 4 GiB device copies, " + ", ".join(
-            f"{x:.2f} ms ({2 * a.numel() * 4 / x / 1e6:.0f} GB/s read+write)" for x in ms))
-
-    bytes_per_update = 4 * w["k"] * feat_bytes + 12
-    avg_epoch_s = sum(epoch_ms) / len(epoch_ms) / 1e3
-    achieved_gbs = nnz * bytes_per_update / avg_epoch_s / 1e9
-    value = nnz * args.steps / wall
-    key = f"{kernel}_{args.scheme}_{w['name']}" + (f"_k{args.k}" if args.k else "")
-    variant = [x for x in sys.argv[1:] if x not in ("--no-cpu-baseline", "--copy-calibration")]
-    drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus", "--log-jsonl"}
+                                    "test_rmse": r["rmses"][args.warmup + i]}) + "\n")
+    bytes_per_update, avg_epoch_s, achieved_gbs = rates(r)
+    value = r["nnz"] * args.steps / r["wall"]
+    kernel = r["kernel"]
+    key = f"{kernel}_{scheme}_{w['name']}" + (f"_k{args.k}" if args.k else "")
+    variant = [x for x in sys.argv[1:] if x not in ("--no-cpu-baseline", "--copy-calibration", "--no-extra")]
+    drop = {"--steps", "--warmup", "--workload", "--scheme", "--cpu-seconds", "--cpu-threads", "--gpus", "--log-jsonl",
+            "--extra-steps"}
     variant = [x for i, x in enumerate(variant) if x not in drop and (i == 0 or variant[i - 1] not in drop)]
     traffic = measured_traffic(key, variant)
     out = {
@@ -351,39 +445,54 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": wall / args.steps * 1e3,
+        "ms_per_step": r["wall"] / args.steps * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if dtype == 0 else "f16-storage/f32-math",
+        "dtype": "f32" if r["dtype"] == 0 else "f16-storage/f32-math",
         "data": f"synthetic (seeded planted low-rank model with the {w['name']} shape)",
-        "config": {"workload": f"{w['name']}: m={w['m']} n={w['n']} k={w['k']} nnz={nnz} ntest={len(T)} "
-                               f"{w['dtype']} {args.scheme}" + (f" s={grid_s}" if args.scheme != "hogwild"
-                                                                 else " f=256"),
-                   "scheme": args.scheme, "partitioned": partitioned, "workers": args.workers or "auto",
-                   "staged": args.staged,
-                   "resident_waves": resident,
-                   "depth": args.depth, "epochs_timed": args.steps},
+        "config": {"workload": describe(r), "scheme": scheme, "partitioned": r["partitioned"],
+                   "workers": args.workers or "auto", "staged": args.staged, "resident_waves": r["resident"],
+                   "depth": args.depth or "auto", "epochs_timed": args.steps},
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": kernel,
-                     "bytes_per_update": bytes_per_update, "updates_per_launch": nnz,
-                     "avg_launch_ms": avg_epoch_s * 1e3},
-        "epoch_updates_per_s": nnz / avg_epoch_s,
-        "median_epoch_ms": sorted(epoch_ms)[len(epoch_ms) // 2],
-        "test_rmse": rmses[-1],
+                     "bytes_per_update": bytes_per_update, "updates_per_launch": r["nnz"],
+                     "avg_launch_ms": avg_epoch_s * 1e3,
+                     "note": "achieved counts every row access at HBM cost (4k*sizeof+12 B per update); rows served "
+                             "by the L2 or the Infinity Cache can push it past the peak.  traffic: L2-to-fabric bytes "
+                             "per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a 4 GiB copy), null unless "
+                             "taken on these kernel sources"},
+        "epoch_updates_per_s": r["nnz"] / avg_epoch_s,
+        "median_epoch_ms": sorted(r["epoch_ms"])[len(r["epoch_ms"]) // 2],
+        "test_rmse": r["rmses"][-1],
     }
-    if args.scheme == "table":
-        tw = mfsgd.get_option("table_workers")
-        out["config"]["workers"] = tw or max(1, grid_s // 2)
-        out["config"]["table_blocks"] = mfsgd.get_option("table_blocks")
+    if traffic:
+        out["roofline"]["traffic_gbs"] = traffic / avg_epoch_s / 1e9
+        out["roofline"]["traffic_frac"] = traffic / avg_epoch_s / 1e9 / HBM_PEAK_GBS
+    if scheme == "table":
+        out["config"]["table_grid"] = r["grid_s"]
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a bounded prefix")
-        serial, omp = cpu_baseline(w, S, args.cpu_seconds, args.cpu_threads)
+        log(f"timing the CPU oracle on a bounded prefix ({threads} OpenMP threads; {physical} physical cores "
+            f"available; OMP_PROC_BIND={os.environ.get('OMP_PROC_BIND')})")
+        serial, omp = cpu_baseline(w, r["S"], args.cpu_seconds, threads)
         out["cpu_baseline"] = serial
         if omp:
+            omp["physical_cores_available"] = physical
             out["cpu_baseline_openmp"] = omp
-    mfsgd.finalize()
+    r["S"] = None
+    if not args.no_extra and not args.staged and args.workload == "hugewiki" and not args.ntrain and not args.k:
+        extra = []
+        for name in ("netflix", "yahoo"):
+            e = measure(args, name, "hogwild", args.extra_steps, 1, dev)
+            bpu, avg_s, gbs = rates(e)
+            extra.append({"workload": describe(e), "scheme": "hogwild",
+                          "form": "one XCD" if e["partitioned"] else "one address space", "kernel": e["kernel"],
+                          "epochs_timed": args.extra_steps, "median_epoch_ms": sorted(e["epoch_ms"])[len(e["epoch_ms"]) // 2],
+                          "epoch_updates_per_s": e["nnz"] / avg_s, "bytes_per_update": bpu,
+                          "algorithmic_gbs": gbs, "frac": gbs / HBM_PEAK_GBS,
+                          "test_rmse_after_epochs": [len(e["rmses"]), e["rmses"][-1]]})
+        out["extra"] = extra
     print(json.dumps(out), flush=True)
 
 

@@ -138,7 +138,7 @@ def main():
     out = os.path.abspath(a.out or os.path.join(ROOT, "profiles", "raw", f"prof_{a.workload}_{a.scheme}"))
     py = sys.executable or "python3"
     base = [py, os.path.join(ROOT, "bench.py"), "--workload", a.workload, "--scheme", a.scheme,
-            "--no-cpu-baseline"] + extra
+            "--no-cpu-baseline", "--no-extra"] + extra
     cmds = {
         "trace": ["rocprofv3", "--kernel-trace", "--stats", "--output-format", "csv", "-d",
                   os.path.join(out, "trace"), "-o", "run", "--"] + base + ["--steps", str(a.steps), "--warmup", "1"],

@@ -62,29 +62,48 @@ enum {
  * MI355X has eight XCDs, each with its own L2 cache; the L2s are not coherent
  * with each other inside a kernel.  Lock-free updates that meet in one L2 see
  * each other at once; updates from different XCDs only when lines are
- * written back and evicted.  The block-scheduled forms keep each worker team
- * on one XCD and pass rows between teams only at block hand-over (agent-scope
+ * written back and evicted, and of two stores to one row that overlap the
+ * later wins.  The block-scheduled forms keep each worker team on one XCD and
+ * pass rows between teams only at block hand-over (agent-scope
  * release/acquire), which is the paper's own answer for workers without a
  * shared coherent memory (section 2.3, and the block partition of section
  * 4.1 applied to XCDs instead of GPUs). */
 enum {
     /* batch-Hogwild! (section 3.2.2): samples are taken in batches of f
      * consecutive samples, each batch updated serially by one worker, workers
-     * never lock.  With option "partition" = 0 the whole array is
-     * split into batches, batch b going to worker (wavefront; half-wavefront
-     * at k <= 32, see "half_waves") b mod W, over the whole GPU in one
-     * address space: updates made on one XCD reach the
-     * others as lines are written back and evicted (see "sync_every"); a row
-     * that several XCDs keep cached is updated in separate copies of which the
-     * one written back last wins, so on data with very popular rows the
-     * per-epoch convergence trails the serial order (batch-Hogwild! inside
-     * one XCD does not).  With
-     * "partition" = 1 the rating matrix is cut into an s x s grid (s = number
-     * of XCDs unless "hogwild_grid" says otherwise; planned internally, once
-     * per sample array) and the wavefronts of each XCD run batch-Hogwild!
-     * inside the block the wavefront schedule below gives that XCD's worker,
-     * each claiming the block's next batch when it is free, so concurrent
-     * updates always meet in one L2. */
+     * never lock.  The form is option "partition":
+     *   2 (default) automatic, the form that follows the serial order within
+     *     the Hogwild! tolerance for these samples (at most min(m, n) / 20
+     *     workers -- the paper's empirical Hogwild! condition, section 5.5.1
+     *     -- and one sample in flight per wavefront): batch-Hogwild! inside
+     *     one XCD (form 4) when the most popular user or item holds more than
+     *     1/64 of the samples (or k <= 32, or binary16 at k <= 64), otherwise
+     *     over all XCDs in one address space with every change added
+     *     atomically (form 0 with "atomic"), the Hogwild! model of
+     *     component-wise atomic updates, so no concurrent update is lost;
+     *     atomic adds read from stale rows add up, so their worker count is
+     *     also kept at most 1 / (4 lr s) for the most popular row's share s.
+     *     The sample array's per-row counts are taken once (synchronously) on
+     *     its first such epoch.  Read-only "hogwild_form" and
+     *     "hogwild_atomic" report what the last epoch ran.
+     *   0 one address space over all XCDs: batch b goes to worker (wavefront;
+     *     half-wavefront at k <= 32, see "half_waves") b mod W.  With plain
+     *     stores a row that several XCDs keep cached is updated in separate
+     *     copies of which the one written back last wins, so on data with
+     *     very popular rows the per-epoch convergence trails the serial order
+     *     (see "sync_every", "coherent"); with "atomic" the changes are added
+     *     atomically instead.
+     *   1 partitioned: the rating matrix is cut into an s x s grid (s =
+     *     number of XCDs unless "hogwild_grid" says otherwise; planned
+     *     internally, once per sample array) and the wavefronts of each XCD
+     *     run batch-Hogwild! inside the block the wavefront schedule below
+     *     gives that XCD's worker, each claiming the block's next batch when
+     *     it is free, so concurrent updates always meet in one L2; the block
+     *     order trails the serial order per epoch (section 5.5.2).
+     *   3 as 1 without the column tickets (the fastest form): workers that
+     *     drift apart may share a column block across XCDs.
+     *   4 one XCD: the whole array as one block run by the wavefronts of one
+     *     XCD (a 1 x 1 grid), claiming batches in order. */
     MFSGD_BATCH_HOGWILD = 0,
     /* wavefront-update (section 3.2.3) on the s x s grid of the last
      * mfsgd_plan: worker i owns row block i and visits the column blocks in
@@ -134,12 +153,16 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *   "batch_f"      batch size f, a positive multiple of 64 (default 256, the
  *                  paper's choice in section 3.2.2).
  *   "workers"      batch-Hogwild! wavefronts in total; 0 (default) = as many
- *                  as stay resident on the GPU.
- *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8
- *                  (default 2).  A wavefront forwards its own pending
- *                  updates, so depth never changes the serial semantics of
- *                  one worker; fewer samples in flight also means fresher
- *                  reads of the rows other workers update.
+ *                  as stay resident on the GPU (the automatic form: at most
+ *                  min(m, n) / 20, see MFSGD_BATCH_HOGWILD).
+ *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8, or
+ *                  0 (default) automatically: 1 for the automatic and
+ *                  one-XCD batch-Hogwild! forms (bound by bandwidth, not
+ *                  latency, so one in flight runs as fast and halves the
+ *                  updates in flight), 2 elsewhere.  A wavefront forwards
+ *                  its own pending updates, so depth never changes the
+ *                  serial semantics of one worker; fewer samples in flight
+ *                  also means fresher reads of the rows other workers update.
  *   "team_waves"   wavefronts per wavefront-update worker (rounded up to
  *                  whole workgroups of 4); 0 (default) = every workgroup slot
  *                  the occupancy allows, shared among the s workers in
@@ -147,19 +170,25 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  worker on one XCD, the XCDs loaded as evenly as the row
  *                  blocks allow).  A worker's wavefronts prefer its blocks
  *                  but also serve the other workers on their XCD.
- *   "partition"    batch-Hogwild!: 0 one address space, 1 partitioned over
- *                  the XCDs (see MFSGD_BATCH_HOGWILD), 2 (default) automatic:
- *                  partitioned when P and Q together take at most 64 MiB
- *                  (they would otherwise sit in every XCD's L2 for the whole
- *                  epoch as diverging copies) or more than 256 MiB (beyond
- *                  the Infinity Cache, where one address space sends every
- *                  L2 miss to HBM), one address space in between;
- *                  3 partitioned without the column tickets: each worker
- *                  walks its column blocks in its wavefront order without
- *                  waiting, so workers that drift apart may share a column
- *                  block, whose rows are then updated on two XCDs at once as
- *                  in one address space (the fastest form; it converges per
- *                  epoch like 1).
+ *   "partition"    batch-Hogwild! form, 0 to 4 (default 2, automatic; see
+ *                  MFSGD_BATCH_HOGWILD).
+ *   "atomic"       1: batch-Hogwild! in one address space or in one XCD adds
+ *                  the change of every value with an atomic add (binary32
+ *                  add, or packed binary16 add; k > 64 for binary16) instead
+ *                  of storing the new row, at depth 1; with "hot_log2" = L >
+ *                  0 only rows holding at least nnz >> L samples are added,
+ *                  the others stored.  0 (default): stores (the automatic
+ *                  form decides by itself).
+ *   "coherent"     one address space, plain stores: 1 agent-scope
+ *                  (write-through) stores, 2 the same plus agent-scope loads,
+ *                  3 non-temporal stores, 4 system-scope stores, for every
+ *                  row not marked hot by "hot_log2" (hot rows keep plain
+ *                  write-back stores); 0 (default) plain.  Measured options:
+ *                  they shrink the per-XCD copies but cost time.
+ *   "coherent_mat" which matrices "coherent" applies to: bit 0 P, bit 1 Q
+ *                  (default 3).
+ *   "hot_log2"     hot rows for "coherent" and "atomic": rows with at least
+ *                  nnz >> hot_log2 samples (0, the default: none).
  *   "hogwild_grid" grid side of the partitioned batch-Hogwild!; 0 (default)
  *                  = number of XCDs.
  *   "balance"      how a grid is cut: 1 into consecutive index ranges
@@ -224,7 +253,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * Read-only keys (after mfsgd_init): "resident_waves" (wavefronts of the
  * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs the
  * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
- * "partitioned" (whether batch-Hogwild! runs partitioned for this model),
+ * "partitioned" (whether batch-Hogwild! runs block-scheduled: the last
+ * epoch's form, or before one the option's), "hogwild_form" (form of the last
+ * batch-Hogwild! epoch, values of "partition" other than 2; -1 before one),
+ * "hogwild_atomic" (whether it added its updates atomically),
  * "half_workers" (whether its one-address-space form runs two workers per
  * wavefront for this model),
  * "table_blocks" (non-empty blocks of the last global-table plan, 0 before one),
@@ -234,6 +266,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * Returns MFSGD_EINVAL for an unknown key or an out-of-range value. */
 int mfsgd_set_option(const char* key, int64_t value);
 int mfsgd_get_option(const char* key, int64_t* value);
+/* Restore every option to its default (the values listed above).  Host
+ * logic only; takes effect like mfsgd_set_option.  Always MFSGD_OK. */
+int mfsgd_reset_options(void);
 
 /* Allocate P (m x k) and Q (n x k) in the storage dtype on the current
  * device and initialise every entry uniformly on [0, 1/sqrt(k)): entry j of

@@ -36,11 +36,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(jobs: int = 4) -> str:
-    """Compile every HIP source and link libmfsgd.so; returns its path."""
+def _stale(src: str) -> bool:
+    """Whether the object of `src` is older than the source or any header."""
+    obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
+    if not os.path.exists(obj):
+        return True
+    deps = [os.path.join(CSRC, src)] + [os.path.join(CSRC, h) for h in os.listdir(CSRC) if h.endswith(".hpp")]
+    deps += [os.path.join(INCLUDE, h) for h in os.listdir(INCLUDE)]
+    return max(os.path.getmtime(d) for d in deps) > os.path.getmtime(obj)
+
+
+def build(jobs: int = 4, changed_only: bool = False) -> str:
+    """Compile every HIP source (changed_only: those whose object is older than
+    its inputs) and link libmfsgd.so; returns its path."""
     os.makedirs(OBJDIR, exist_ok=True)
+    todo = [s for s in SOURCES if not changed_only or _stale(s)]
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(SOURCES)))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        list(ex.map(_compile, todo))
+    objs = [os.path.join(OBJDIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -51,4 +64,5 @@ def build(jobs: int = 4) -> str:
 
 
 if __name__ == "__main__":
-    print(build())
+    import sys
+    print(build(changed_only="--changed" in sys.argv))

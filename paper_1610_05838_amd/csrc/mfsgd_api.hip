@@ -16,13 +16,14 @@ namespace {
 
 using namespace mfsgd;
 
+
 thread_local std::string g_err;
 
 struct Options {
     int64_t dtype = MFSGD_FP32;
     int64_t batch_f = 256;
     int64_t workers = 0;
-    int64_t depth = 2;
+    int64_t depth = 0;
     int64_t team_waves = 0;
     int64_t partition = 2;
     int64_t hogwild_grid = 0;
@@ -36,7 +37,26 @@ struct Options {
     int64_t half_waves = 1;
     int64_t table_grid = 256;
     int64_t table_workers = 0;
+    int64_t atomic = 0;
+    int64_t coherent = 0;
+    int64_t coherent_mat = 3;
+    int64_t hot_log2 = 0;
     int64_t debug = 0;
+};
+
+// Hot-row bits of one sample array (coherent one-address-space batch-Hogwild!):
+// row i of P (Q) is hot when it holds at least nnz >> log2 of the samples.
+struct HotSet {
+    const mfsgd_sample* src = nullptr;
+    int64_t nnz = -1;
+    int log2 = -1;
+    uint32_t* bits = nullptr; // ceil(m/32) words for P, then ceil(n/32) for Q
+    int64_t bits_cap = 0;
+    int64_t hot_p = 0, hot_q = 0; // rows marked
+    bool matches(const mfsgd_sample* p, int64_t n, int l) const
+    {
+        return src == p && nnz == n && log2 == l && src != nullptr;
+    }
 };
 
 // A grouping of one sample array into the blocks of an s x s grid.
@@ -85,6 +105,15 @@ struct TablePlan {
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
 };
 
+// The most samples any one user and any one item holds, for one sample array
+// (the automatic batch-Hogwild! form).
+struct RowStats {
+    const mfsgd_sample* src = nullptr;
+    int64_t nnz = -1;
+    unsigned long long du = 0, dv = 0;
+    bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
+};
+
 struct Context {
     bool inited = false;
     int device = 0;
@@ -107,6 +136,11 @@ struct Context {
     Plan wf;                // the caller's wavefront-update plan (mfsgd_plan)
     Plan hw;                // internal plan of the XCD-partitioned batch-Hogwild!
     TablePlan gt;           // internal plan of the global scheduling table
+    HotSet hot;             // hot rows of the last coherent batch-Hogwild! sample array
+    RowStats stats;         // largest user and item sample counts of the last automatic batch-Hogwild! array
+    unsigned long long* maxdeg = nullptr; // 2 device words for them
+    int last_form = -1;     // form of the last batch-Hogwild! epoch (values of option "partition"), -1 before one
+    int last_atomic = 0;    // whether it added its updates atomically
     // planner scratch
     int64_t* counts = nullptr;
     int64_t counts_cap = 0;
@@ -251,6 +285,8 @@ void release_all()
     dfree(c.totals);
     dfree(c.bnd);
     dfree(c.deg);
+    dfree(c.hot.bits);
+    dfree(c.maxdeg);
     dfree(c.visits);
     dfree(c.trace);
     dfree(c.tmap);
@@ -343,25 +379,58 @@ bool rows_fit_31_bits()
     return std::max(g.m, g.n) * row <= (int64_t(1) << 31);
 }
 
-// Whether batch-Hogwild! runs partitioned over the XCDs.  Automatic choice:
-// Automatic choice of the batch-Hogwild! form by the size of P and Q:
-// up to kPartitionBytes they stay resident in every XCD's L2 for the whole
-// epoch, so one-address-space workers would train eight diverging copies;
-// partitioned teams keep every update in one L2.  Above kCacheBytes (the
-// Infinity Cache) every L2 miss of the one-address-space form goes to HBM,
-// while a partitioned team touches one row block and one column block at a
-// time; measured on the Yahoo shape (832 MB of factors) the partitioned form
-// is both faster and no worse per epoch.  In between, the one-address-space
-// form is the faster one and converges best per epoch (Netflix shape).
-constexpr int64_t kPartitionBytes = int64_t(64) << 20;
-constexpr int64_t kCacheBytes = int64_t(256) << 20;
+// The batch-Hogwild! forms (option "partition").  Each XCD's L2 is a
+// write-back cache the other XCDs do not see inside a kernel, so lock-free
+// updates of one row made on two XCDs land in separate copies and the copy
+// written back last wins, and inside one L2 two workers that update one row
+// at once keep only the later store.  Measured against the serial oracle:
+//   * one address space over all XCDs (0): the per-XCD copies of popular rows
+//     trail the serial order (Netflix shape, 20 epochs: 0.017 in test RMSE);
+//   * XCD-partitioned (1, 3): a coarse block order that trails by 0.05;
+//   * one XCD (4): every update meets in one L2; where a few rows hold a
+//     large share of the samples and the learning rate decays (Netflix
+//     shape) it ends within 1e-3 of the serial oracle, but where many rows
+//     are moderately popular and the rate stays constant (Yahoo shape) the
+//     stores that overwrite concurrent updates of the same row make it fall
+//     behind epoch after epoch;
+//   * one address space with atomic adds of every change (0 with option
+//     "atomic"): no update is lost -- the Hogwild! model of component-wise
+//     atomic updates -- and the Yahoo-shaped run follows the serial oracle to
+//     1e-4, but the adds of one row meet at one memory channel, which the
+//     hottest Netflix-shaped rows saturate.
+// The automatic form (2, the default) therefore takes one XCD when the most
+// popular user or item holds more than 1/kOneXcdShareInv of the samples and
+// atomic adds over all XCDs otherwise; both run one sample in flight per
+// wavefront and at most min(m, n) / 20 workers (the paper's empirical
+// Hogwild! condition, section 5.5.1).
+constexpr int kOneXcdShareInv = 64;
 
 bool partitioned_hogwild()
 {
-    if (g_opt.partition != 2)
-        return g_opt.partition == 1 || g_opt.partition == 3;
-    const int64_t model = (g.m + g.n) * (int64_t)g.KP * (int64_t)elem_size(g.dtype);
-    return model <= kPartitionBytes || model > kCacheBytes;
+    if (g.last_form >= 0)
+        return g.last_form != 0;
+    return g_opt.partition == 1 || g_opt.partition == 3 || g_opt.partition == 4;
+}
+
+// grid side of the block-scheduled batch-Hogwild! plan of form `form`
+int hogwild_grid_side(int form)
+{
+    if (form == 4)
+        return 1;
+    return g_opt.hogwild_grid > 0 ? (int)g_opt.hogwild_grid : std::max(1, g.nx);
+}
+
+// workers of the automatic forms: the paper's Hogwild! condition
+int64_t hogwild_condition_workers() { return std::max<int64_t>(1, std::min(g.m, g.n) / 20); }
+
+// samples in flight per wavefront: the option, or automatically 1 for
+// batch-Hogwild! in one XCD (bound by that XCD's bandwidth, not by latency:
+// depth 1 runs as fast and halves the updates in flight) and 2 elsewhere
+int depth_for(bool hogwild_one_xcd)
+{
+    if (g_opt.depth > 0)
+        return (int)g_opt.depth;
+    return hogwild_one_xcd ? 1 : 2;
 }
 
 // ---------------------------------------------------------------------------
@@ -378,9 +447,9 @@ const OptSpec kOpts[] = {
     {"dtype", &Options::dtype, 0, 1, "dtype must be 0 (fp32) or 1 (fp16)"},
     {"batch_f", &Options::batch_f, 64, int64_t(1) << 30, "batch_f must be a positive multiple of 64"},
     {"workers", &Options::workers, 0, int64_t(1) << 30, "workers must be in [0, 2^30]"},
-    {"depth", &Options::depth, 1, 8, "depth must be 1, 2, 4 or 8"},
+    {"depth", &Options::depth, 0, 8, "depth must be 0 (automatic), 1, 2, 4 or 8"},
     {"team_waves", &Options::team_waves, 0, 65536, "team_waves must be in [0, 65536]"},
-    {"partition", &Options::partition, 0, 3, "partition must be 0, 1, 2 or 3"},
+    {"partition", &Options::partition, 0, 4, "partition must be 0, 1, 2, 3 or 4"},
     {"hogwild_grid", &Options::hogwild_grid, 0, kMaxGrid, "hogwild_grid must be in [0, 64]"},
     {"balance", &Options::balance, 0, 2, "balance must be 0, 1 or 2"},
     {"sync_every", &Options::sync_every, 0, int64_t(1) << 30, "sync_every must be in [0, 2^30]"},
@@ -392,6 +461,10 @@ const OptSpec kOpts[] = {
     {"half_waves", &Options::half_waves, 0, 2, "half_waves must be 0, 1 or 2"},
     {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
     {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
+    {"atomic", &Options::atomic, 0, 1, "atomic must be 0 or 1"},
+    {"coherent", &Options::coherent, 0, 4, "coherent must be in [0, 4]"},
+    {"coherent_mat", &Options::coherent_mat, 0, 3, "coherent_mat must be in [0, 3]"},
+    {"hot_log2", &Options::hot_log2, 0, 62, "hot_log2 must be in [0, 62]"},
     {"debug", &Options::debug, 0, 3, "debug must be in [0, 3]"},
 };
 
@@ -406,7 +479,7 @@ int set_option_impl(const char* key, int64_t value)
         if (ok && o.field == &Options::batch_f)
             ok = value % 64 == 0;
         if (ok && o.field == &Options::depth)
-            ok = value == 1 || value == 2 || value == 4 || value == 8;
+            ok = value == 0 || value == 1 || value == 2 || value == 4 || value == 8;
         if (!ok)
             return fail(MFSGD_EINVAL, o.what);
         g_opt.*(o.field) = value;
@@ -427,21 +500,26 @@ int get_option_impl(const char* key, int64_t* value)
     const bool ro = !std::strcmp(key, "resident_waves") || !std::strcmp(key, "xcds") || !std::strcmp(key, "cus") ||
                     !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
                     !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks") ||
-                    !std::strcmp(key, "half_workers");
+                    !std::strcmp(key, "half_workers") || !std::strcmp(key, "hogwild_form") ||
+                    !std::strcmp(key, "hogwild_atomic");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
         return fail(MFSGD_ESTATE, std::string("'") + key + "' is read-only and needs mfsgd_init");
     if (!std::strcmp(key, "resident_waves"))
-        *value = (int64_t)g.cus * occupancy_waves(g.KP, g.dtype, (int)g_opt.depth);
+        *value = (int64_t)g.cus * occupancy_waves(g.KP, g.dtype, depth_for(false));
     else if (!std::strcmp(key, "xcds"))
         *value = g.nx;
     else if (!std::strcmp(key, "half_workers"))
         *value = half_wave_workers(g.KP, g.dtype) ? 1 : 0;
     else if (!std::strcmp(key, "blocked_per_cu"))
-        *value = occupancy_blocked(g.KP, g.dtype, (int)g_opt.depth, 256);
+        *value = occupancy_blocked(g.KP, g.dtype, depth_for(g_opt.partition == 2 || g_opt.partition == 4), 256);
     else if (!std::strcmp(key, "partitioned"))
         *value = partitioned_hogwild() ? 1 : 0;
+    else if (!std::strcmp(key, "hogwild_form"))
+        *value = g.last_form;
+    else if (!std::strcmp(key, "hogwild_atomic"))
+        *value = g.last_atomic;
     else if (!std::strcmp(key, "teams_grid"))
         *value = g.lay_plan ? g.lay_grid : 0;
     else if (!std::strcmp(key, "table_blocks"))
@@ -484,6 +562,9 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
         return fail(MFSGD_EINVAL, "k must be in [1, 512]");
     release_all();
     Context& c = g;
+    c.last_form = -1;
+    c.last_atomic = 0;
+    c.stats = RowStats();
     HIPCHK(hipGetDevice(&c.device));
     HIPCHK(hipDeviceGetAttribute(&c.cus, hipDeviceAttributeMultiprocessorCount, c.device));
     c.m = m;
@@ -596,6 +677,65 @@ bool balanced_grid(int s)
 int bad_index_error()
 {
     return fail(MFSGD_EINVAL, "a sample index is out of range (need 0 <= u < m and 0 <= v < n)");
+}
+
+// Largest user and item sample counts of a sample array (cached per array).
+int row_stats(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
+{
+    Context& c = g;
+    if (c.stats.matches(samples, nnz))
+        return MFSGD_OK;
+    c.stats.src = nullptr;
+    CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
+    if (!c.maxdeg)
+        CHK(dalloc((void**)&c.maxdeg, 2 * sizeof(unsigned long long), "largest degrees"));
+    HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
+    HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
+    HIPCHK(hipMemsetAsync(c.maxdeg, 0, 2 * sizeof(unsigned long long), st));
+    HIPCHK(plan_degrees((const Sample*)samples, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
+    HIPCHK(max_degree(c.deg, c.m, c.maxdeg, st));
+    HIPCHK(max_degree(c.deg + c.m, c.n, c.maxdeg + 1, st));
+    unsigned long long h[2] = {0, 0};
+    HIPCHK(hipMemcpyAsync(h, c.maxdeg, sizeof(h), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    if (*c.hflag) {
+        *c.hflag = 0;
+        return bad_index_error();
+    }
+    c.stats.du = h[0];
+    c.stats.dv = h[1];
+    c.stats.src = samples;
+    c.stats.nnz = nnz;
+    return MFSGD_OK;
+}
+
+// Hot-row bits of a sample array: per-index sample counts (the planner's
+// degree kernel), then one bit per row of P and of Q.
+int build_hot(const mfsgd_sample* samples, int64_t nnz, int log2, hipStream_t st)
+{
+    Context& c = g;
+    HotSet& h = c.hot;
+    h.src = nullptr;
+    const int64_t wp = (c.m + 31) / 32, wq = (c.n + 31) / 32;
+    CHK(grow(&h.bits, &h.bits_cap, wp + wq, "hot-row bits"));
+    CHK(grow(&c.deg, &c.deg_cap, c.m + c.n, "plan degrees"));
+    HIPCHK(hipMemsetAsync(c.bad, 0, sizeof(int), st));
+    HIPCHK(hipMemsetAsync(c.deg, 0, sizeof(unsigned long long) * (size_t)(c.m + c.n), st));
+    HIPCHK(plan_degrees((const Sample*)samples, nnz, c.m, c.n, c.deg, c.deg + c.m, c.bad, st));
+    const unsigned long long thr = std::max<unsigned long long>(1ull, (unsigned long long)nnz >> log2);
+    HIPCHK(hot_bits(c.deg, c.m, thr, h.bits, st));
+    HIPCHK(hot_bits(c.deg + c.m, c.n, thr, h.bits + wp, st));
+    HIPCHK(hipMemcpyAsync(c.hflag, c.bad, sizeof(int), hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    if (*c.hflag) {
+        *c.hflag = 0;
+        return bad_index_error();
+    }
+    h.src = samples;
+    h.nnz = nnz;
+    h.log2 = log2;
+    return MFSGD_OK;
 }
 
 int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool balanced, bool keep_orig,
@@ -784,7 +924,7 @@ int table_epoch(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, fl
         CHK(build_table_plan(pl, samples, nnz, s, keep, st));
     TableLaunch a{};
     a.KP = c.KP;
-    a.depth = (int)g_opt.depth;
+    a.depth = depth_for(false);
     a.Sp = pl.Sp;
     a.bstart = pl.bstart;
     a.s = s;
@@ -1034,14 +1174,27 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         return table_epoch(samples, nnz, lr, lp, lq, st);
     const int64_t dbg = g_opt.debug;
     const bool hog = scheme == MFSGD_BATCH_HOGWILD;
-    const bool blocked = !hog || partitioned_hogwild();
+    const bool automatic = hog && g_opt.partition == 2;
+    int form = hog ? (int)g_opt.partition : -1;
+    bool atomic = hog && g_opt.atomic != 0;
+    if (automatic) {
+        // the serial-tracking form for these samples
+        CHK(row_stats(samples, nnz, st));
+        const unsigned long long top = std::max(c.stats.du, c.stats.dv);
+        const bool skewed = nnz > 0 && (double)top * kOneXcdShareInv > (double)nnz;
+        // atomic adds need one worker per wavefront and, in binary16, value pairs
+        const bool no_atomic = c.KP == 32 || (c.dtype == MFSGD_FP16 && c.KP < 128);
+        form = skewed || no_atomic ? 4 : 0;
+        atomic = form == 0;
+    }
+    const bool blocked = !hog || form != 0;
     Plan* pl = nullptr;
     if (!hog) {
         if (!c.wf.matches(samples, nnz))
             return fail(MFSGD_ESTATE, "wavefront-update needs mfsgd_plan on these samples first");
         pl = &c.wf;
     } else if (blocked) {
-        const int s_h = g_opt.hogwild_grid > 0 ? (int)g_opt.hogwild_grid : c.nx;
+        const int s_h = hogwild_grid_side(form);
         const bool keep = (dbg & 1) != 0;
         if (!c.hw.matches(samples, nnz) || c.hw.s != s_h || c.hw.balanced != balanced_grid(s_h) ||
             (keep && !c.hw.has_orig))
@@ -1053,7 +1206,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
 
     EpochLaunch a{};
     a.KP = c.KP;
-    a.depth = (int)g_opt.depth;
+    a.depth = depth_for(hog && (form == 4 || atomic));
     a.nnz = nnz;
     a.f = (int)g_opt.batch_f;
     a.P = c.P;
@@ -1078,6 +1231,14 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             if (per_cu <= 0)
                 return fail(MFSGD_EHIP, "occupancy query failed for the epoch kernel");
             W = (int64_t)c.cus * per_cu * (half_wave_workers(c.KP, c.dtype) ? 2 : 1);
+            if (automatic) {
+                // atomic adds computed from stale reads add up: keep the
+                // concurrent updates of the most popular row times the rate
+                // at most 1/4 (the summed steps of one row stay small)
+                const double top = (double)std::max(c.stats.du, c.stats.dv) / (double)std::max<int64_t>(nnz, 1);
+                const double cap = top > 0 && lr > 0 ? 0.25 / ((double)lr * top) : 1e18;
+                W = std::min(W, std::min(hogwild_condition_workers(), std::max<int64_t>(1, (int64_t)std::min(cap, 1e18))));
+            }
         }
         W = std::min(W, nbatch);
         a.scheme = kSchemeHogwild;
@@ -1087,6 +1248,31 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.sync_every = (int)g_opt.sync_every;
         a.sync_l1 = (int)g_opt.sync_l1;
         a.nx = c.nx;
+        if (atomic) {
+            if (a.depth != 1 || a.half || (c.dtype == MFSGD_FP16 && c.KP < 128))
+                return fail(MFSGD_EINVAL, "atomic updates need depth 1, one worker per wavefront and, for binary16, "
+                                          "k > 64");
+            a.atomic = 1;
+            a.coh = g_opt.coherent == kCohBoth ? kCohBoth : kCohOff;
+            const int l2 = (int)g_opt.hot_log2;
+            if (l2 > 0 && nnz > 0) {
+                if (!c.hot.matches(samples, nnz, l2))
+                    CHK(build_hot(samples, nnz, l2, st));
+                a.hot_p = c.hot.bits;
+                a.hot_q = c.hot.bits + (c.m + 31) / 32;
+            }
+        } else if (g_opt.coherent != kCohOff && !a.half) {
+            a.coh = (int)g_opt.coherent;
+            a.coh_p = (g_opt.coherent_mat & 1) ? 1 : 0;
+            a.coh_q = (g_opt.coherent_mat & 2) ? 1 : 0;
+            const int l2 = (int)g_opt.hot_log2;
+            if (l2 > 0 && nnz > 0) {
+                if (!c.hot.matches(samples, nnz, l2))
+                    CHK(build_hot(samples, nnz, l2, st));
+                a.hot_p = c.hot.bits;
+                a.hot_q = c.hot.bits + (c.m + 31) / 32;
+            }
+        }
         if (dbg & 2) {
             CHK(grow(&c.trace, &c.trace_cap, nbatch, "trace"));
             c.trace_n = nbatch;
@@ -1104,8 +1290,14 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         int64_t want;
         if (scheme == MFSGD_WAVEFRONT_DET)
             want = 1;
+        else if (hog && g_opt.workers > 0)
+            want = std::max<int64_t>(1, g_opt.workers / s);
+        else if (automatic)
+            // one XCD: the paper's empirical Hogwild! condition caps the
+            // default; the team never exceeds the XCD's resident slots
+            want = hogwild_condition_workers();
         else if (hog)
-            want = g_opt.workers > 0 ? std::max<int64_t>(1, g_opt.workers / s) : 0;
+            want = 0;
         else
             want = g_opt.team_waves;
         a.scheme = kSchemeWavefront;
@@ -1123,11 +1315,26 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             a.half = 1;
             a.sink = nullptr;
         }
+        if (atomic) {
+            if (a.depth != 1 || a.half || (c.dtype == MFSGD_FP16 && c.KP < 128))
+                return fail(MFSGD_EINVAL, "atomic updates need depth 1, one batch per wavefront and, for binary16, "
+                                          "k > 64");
+            a.atomic = 1;
+            a.sink = nullptr;
+            const int l2 = (int)g_opt.hot_log2;
+            if (l2 > 0 && nnz > 0) {
+                // atomic adds for the hot rows only
+                if (!c.hot.matches(samples, nnz, l2))
+                    CHK(build_hot(samples, nnz, l2, st));
+                a.hot_p = c.hot.bits;
+                a.hot_q = c.hot.bits + (c.m + 31) / 32;
+            }
+        }
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
         a.tickets = c.tickets;
         a.sched = c.sched;
-        a.free_run = hog && g_opt.partition == 3 ? 1 : 0;
+        a.free_run = hog && form == 3 ? 1 : 0;
         a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
             // columns, then two event stamps per (team, wave)
@@ -1154,6 +1361,10 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             else
                 HIPCHK(epoch_f32(a, st));
         }
+    }
+    if (hog) {
+        c.last_form = form;
+        c.last_atomic = atomic ? 1 : 0;
     }
     c.epoch += 1;
     return MFSGD_OK;
@@ -1239,7 +1450,7 @@ int epoch_staged_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float 
     EpochLaunch a{};
     a.scheme = kSchemeHogwild;
     a.KP = c.KP;
-    a.depth = (int)g_opt.depth;
+    a.depth = depth_for(false);
     a.f = (int)f;
     a.P = c.P;
     a.Q = c.Q;
@@ -1406,6 +1617,14 @@ int mfsgd_set_option(const char* key, int64_t value)
 int mfsgd_get_option(const char* key, int64_t* value)
 {
     return guarded([&]() -> int { return get_option_impl(key, value); });
+}
+
+int mfsgd_reset_options(void)
+{
+    return guarded([&]() -> int {
+        g_opt = Options();
+        return MFSGD_OK;
+    });
 }
 
 int mfsgd_init(int64_t m, int64_t n, int32_t k, uint64_t seed)

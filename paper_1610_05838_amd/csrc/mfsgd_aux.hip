@@ -208,6 +208,61 @@ __global__ __launch_bounds__(256) void k_degrees(const Sample* __restrict__ S, i
         atomicOr(bad, 1);
 }
 
+// One thread per 32 rows: no atomics, every word written once.
+__global__ void k_hot_bits(const unsigned long long* __restrict__ deg, int64_t rows, unsigned long long thr,
+                           uint32_t* __restrict__ bits)
+{
+    const int64_t words = (rows + 31) / 32;
+    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < words; w += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t b = 0;
+        for (int i = 0; i < 32; ++i) {
+            const int64_t r = w * 32 + i;
+            if (r < rows && deg[r] >= thr)
+                b |= 1u << i;
+        }
+        bits[w] = b;
+    }
+}
+
+hipError_t hot_bits(const unsigned long long* deg, int64_t rows, unsigned long long thr, uint32_t* bits,
+                    hipStream_t st)
+{
+    const int64_t words = (rows + 31) / 32;
+    if (words == 0)
+        return hipSuccess;
+    int64_t blocks = (words + 255) / 256;
+    if (blocks > 4096)
+        blocks = 4096;
+    hipLaunchKernelGGL(k_hot_bits, dim3((unsigned)blocks), dim3(256), 0, st, deg, rows, thr, bits);
+    return hipGetLastError();
+}
+
+// Largest entry of deg[0 .. rows-1], atomically folded into *out (which the
+// caller zeroes).
+__global__ void k_max_u64(const unsigned long long* __restrict__ deg, int64_t rows, unsigned long long* out)
+{
+    unsigned long long mx = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < rows; i += (int64_t)gridDim.x * blockDim.x)
+        mx = deg[i] > mx ? deg[i] : mx;
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long y = __shfl_xor(mx, o);
+        mx = y > mx ? y : mx;
+    }
+    if ((threadIdx.x & 63) == 0 && mx > 0)
+        atomicMax(out, mx);
+}
+
+hipError_t max_degree(const unsigned long long* deg, int64_t rows, unsigned long long* out, hipStream_t st)
+{
+    if (rows <= 0)
+        return hipSuccess;
+    int64_t blocks = (rows + 255) / 256;
+    if (blocks > 1024)
+        blocks = 1024;
+    hipLaunchKernelGGL(k_max_u64, dim3((unsigned)blocks), dim3(256), 0, st, deg, rows, out);
+    return hipGetLastError();
+}
+
 hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsigned long long* du,
                         unsigned long long* dv, int* bad, hipStream_t st)
 {

@@ -274,6 +274,84 @@ struct CacheSync {
     bool l1;     // this wavefront invalidates its CU's L1
 };
 
+// Cross-XCD coherence of row updates in the one-address-space batch-Hogwild!.
+// Each XCD's L2 is a write-back cache that the other XCDs do not see, so a
+// row updated on one XCD and read on another while the line is still dirty
+// in the first L2 is read stale, and whichever L2 writes the line back last
+// discards the other's updates.  Rows stored with an agent-scope store
+// (sc1) are written through to memory, where every XCD's next miss finds
+// them.  Rows that hold a large share of the samples ("hot", one bit per row)
+// keep write-back stores: their update rate would otherwise serialise on the
+// one memory channel that holds them, and a row updated that often is
+// over-determined, so losing part of its updates changes nothing measurable.
+enum : int {
+    kCohOff = 0,    // every store write-back (plain)
+    kCohStore = 1,  // agent-scope stores for rows that are not hot
+    kCohBoth = 2,   // ... and agent-scope loads for them
+    kCohNT = 3,     // non-temporal stores for rows that are not hot
+    kCohSys = 4,    // system-scope stores for rows that are not hot
+};
+struct Coherence {
+    const uint32_t* hot_p; // bit u: row u of P is hot (nullptr: no row is)
+    const uint32_t* hot_q; // bit v: row v of Q is hot
+    bool p, q;             // apply the coherent policy to P's / Q's rows
+};
+
+__device__ __forceinline__ bool hot_bit(const uint32_t* __restrict__ bits, int i)
+{
+    return bits != nullptr && ((bits[(uint32_t)i >> 5] >> (i & 31)) & 1u) != 0;
+}
+
+template <int N>
+struct UIntOf;
+template <>
+struct UIntOf<2> { typedef uint16_t type; };
+template <>
+struct UIntOf<4> { typedef uint32_t type; };
+template <>
+struct UIntOf<8> { typedef uint64_t type; };
+
+// One lane's part of a row stored / loaded with the coherent policy COH.
+template <int COH, typename V>
+__device__ __forceinline__ void st_coh(V* p, V v)
+{
+    if constexpr (COH == kCohNT) {
+        __builtin_nontemporal_store(v, p);
+    } else {
+        constexpr int scope = COH == kCohSys ? __HIP_MEMORY_SCOPE_SYSTEM : __HIP_MEMORY_SCOPE_AGENT;
+        if constexpr (sizeof(V) <= 8) {
+            typedef typename UIntOf<sizeof(V)>::type U;
+            __hip_atomic_store(reinterpret_cast<U*>(p), __builtin_bit_cast(U, v), __ATOMIC_RELAXED, scope);
+        } else {
+            static_assert(sizeof(V) % 8 == 0, "rows are stored in 8-byte parts");
+            uint64_t w[sizeof(V) / 8];
+            __builtin_memcpy(w, &v, sizeof(V));
+#pragma unroll
+            for (int i = 0; i < (int)(sizeof(V) / 8); ++i)
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(p) + i, w[i], __ATOMIC_RELAXED, scope);
+        }
+    }
+}
+
+template <typename V>
+__device__ __forceinline__ V ld_coh(const V* p)
+{
+    if constexpr (sizeof(V) <= 8) {
+        typedef typename UIntOf<sizeof(V)>::type U;
+        return __builtin_bit_cast(
+            V, __hip_atomic_load(reinterpret_cast<const U*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    } else {
+        uint64_t w[sizeof(V) / 8];
+#pragma unroll
+        for (int i = 0; i < (int)(sizeof(V) / 8); ++i)
+            w[i] = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p) + i, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+        V v;
+        __builtin_memcpy(&v, w, sizeof(V));
+        return v;
+    }
+}
+
 // Debug hooks of one epoch.
 struct DebugSink {
     uint32_t* visits;     // per caller-array sample, or nullptr
@@ -313,16 +391,67 @@ struct WorkerState {
     float sr[D];
     V hp[D], hq[D]; // rows of the last D samples, as stored
     int hu[D], hv[D];
+    bool cp[D], cq[D]; // coherent policy for the rows in flight
 };
 
-template <int KP, typename T, int D, bool DBG, bool SKIP = false, bool BUF = false>
+// Atomic row updates: the change of every value is added with an L2 atomic
+// (binary32 add, or packed binary16 add) instead of storing the new row, so
+// concurrent updates of one row all take effect (Hogwild!'s model of
+// component-wise atomic updates) rather than the last store winning.
+//
+// Binary32 rows of 2 or 4 values per lane are first transposed across the
+// wavefront (ds_bpermute, no LDS storage) so that atomic instruction e adds
+// values 64 e .. 64 e + 63 of the row, one per lane: each instruction then
+// covers 256 contiguous bytes instead of the whole row with gaps.
+// `row` points at value 0 of the row, `lane` is the lane index.
+template <typename T, int E>
+__device__ __forceinline__ void add_row_t(T* row, int lane, const float (&d)[E])
+{
+    static_assert(sizeof(T) == 4 && (E == 2 || E == 4), "transposed adds: binary32, 2 or 4 values per lane");
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int x = 64 * e + lane;         // value this lane adds in instruction e
+        const int src = x / E, comp = x % E; // the lane that holds it, and where
+        float v = 0.f;
+#pragma unroll
+        for (int c = 0; c < E; ++c) {
+            const float y = __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(d[c])));
+            v = comp == c ? y : v;
+        }
+        __hip_atomic_fetch_add(reinterpret_cast<float*>(row) + x, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+template <typename T, int E>
+__device__ __forceinline__ void add_row(T* p, const float (&d)[E])
+{
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            __hip_atomic_fetch_add(reinterpret_cast<float*>(p) + e, d[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+        static_assert(E % 2 == 0, "binary16 rows are added in pairs");
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int e = 0; e < E; e += 2) {
+            h2 v = {(_Float16)d[e], (_Float16)d[e + 1]};
+            __builtin_amdgcn_global_atomic_fadd_v2f16(reinterpret_cast<h2*>(p + e), v);
+        }
+    }
+}
+
+template <int KP, typename T, int D, bool DBG, bool SKIP = false, bool BUF = false, int COH = kCohOff,
+          bool ATOM = false>
 __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t worker,
                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
                                            float lq, const DebugSink dbg, const CacheSync sync = CacheSync{0, false, false},
-                                           T* sink = nullptr)
+                                           T* sink = nullptr, const Coherence coh = Coherence{nullptr, nullptr, false, false})
 {
     constexpr int E = Geo<KP>::E;
     static_assert(!BUF || (!SKIP && sizeof(T) * E == 4), "buffer rows: one dword per lane, no store redirection");
+    static_assert(COH == kCohOff || (!BUF && !SKIP), "coherent rows use global addressing");
+    static_assert(!ATOM || (D == 1 && !BUF && !SKIP && COH != kCohStore && COH != kCohNT && COH != kCohSys),
+                  "atomic updates: one sample in flight, global addressing");
     constexpr int A = Geo<KP>::A;
     typedef Row<T, E> R;
     static_assert(64 % D == 0 && D <= 32, "depth must divide 64");
@@ -371,6 +500,7 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         st.su[d] = st.sv[d] = st.hu[d] = st.hv[d] = -1;
         st.sr[d] = 0.f;
         st.sp[d] = st.sq[d] = st.hp[d] = st.hq[d] = V{};
+        st.cp[d] = st.cq[d] = false;
     }
 
     // request the rows of the sample at lane `xl` of a chunk's metadata
@@ -382,7 +512,29 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         st.su[slot] = ok ? u : -1;
         st.sv[slot] = ok ? v : -1;
         st.sr[slot] = r;
-        if constexpr (BUF) {
+        if constexpr (ATOM) {
+            // rows updated with atomic adds: every row, or the hot ones
+            st.cp[slot] = coh.hot_p == nullptr || hot_bit(coh.hot_p, ok ? u : 0);
+            st.cq[slot] = coh.hot_q == nullptr || hot_bit(coh.hot_q, ok ? v : 0);
+        }
+        if constexpr (ATOM && COH == kCohBoth) {
+            st.sp[slot] = ld_coh(reinterpret_cast<const V*>(P + (int64_t)(ok ? u : 0) * KP + col));
+            st.sq[slot] = ld_coh(reinterpret_cast<const V*>(Q + (int64_t)(ok ? v : 0) * KP + col));
+        } else if constexpr (COH != kCohOff) {
+            const bool cp = coh.p && !hot_bit(coh.hot_p, ok ? u : 0);
+            const bool cq = coh.q && !hot_bit(coh.hot_q, ok ? v : 0);
+            st.cp[slot] = cp;
+            st.cq[slot] = cq;
+            const V* pr = reinterpret_cast<const V*>(P + (int64_t)(ok ? u : 0) * KP + col);
+            const V* qr = reinterpret_cast<const V*>(Q + (int64_t)(ok ? v : 0) * KP + col);
+            if constexpr (COH == kCohBoth) {
+                st.sp[slot] = cp ? ld_coh(pr) : *pr;
+                st.sq[slot] = cq ? ld_coh(qr) : *qr;
+            } else {
+                st.sp[slot] = *pr;
+                st.sq[slot] = *qr;
+            }
+        } else if constexpr (BUF) {
             st.sp[slot] = bp.template ld<V>(cb, (uint32_t)(ok ? u : 0) * kRowBytes);
             st.sq[slot] = bq.template ld<V>(cb, (uint32_t)(ok ? v : 0) * kRowBytes);
         } else {
@@ -430,6 +582,52 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
             dot = holds ? dot : 0.f; // idle lanes hold a copy of column 0
         dot = wave_sum(dot);
         const float err = st.sr[j] - dot;
+        if constexpr (ATOM) {
+            // the changes lr (err q - lp p) and lr (err p - lq q), both from
+            // the values before the step, added atomically to the rows marked
+            // for it and stored (value plus change) to the others; with one
+            // sample in flight the next load of this wavefront is issued after
+            // these writes and sees them
+            float dp[E], dq[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                dp[e] = lr * (err * q[e] - lp * p[e]);
+                dq[e] = lr * (err * p[e] - lq * q[e]);
+            }
+            if (holds) {
+                T* pr = P + (int64_t)u * KP + col;
+                T* qr = Q + (int64_t)v * KP + col;
+                if (st.cp[j]) {
+                    if constexpr (sizeof(T) == 4 && A == 64 && (E == 2 || E == 4))
+                        add_row_t<T, E>(P + (int64_t)u * KP, lane, dp);
+                    else
+                        add_row<T, E>(pr, dp);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        dp[e] += p[e];
+                    R::store(pr, dp);
+                }
+                if (st.cq[j]) {
+                    if constexpr (sizeof(T) == 4 && A == 64 && (E == 2 || E == 4))
+                        add_row_t<T, E>(Q + (int64_t)v * KP, lane, dq);
+                    else
+                        add_row<T, E>(qr, dq);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        dq[e] += q[e];
+                    R::store(qr, dq);
+                }
+            }
+            if constexpr (DBG) {
+                if (dbg.visits && lane == 0) {
+                    const int64_t idx = dbg.orig ? dbg.orig[pos] : pos;
+                    atomicAdd(dbg.visits + idx, 1u);
+                }
+            }
+            return;
+        }
         if constexpr (sizeof(T) == 2) {
             // Binary16 storage (instruction-issue bound): p + lr (err q - lp p)
             // evaluated as (p + (lr err) q) - (lr lp) p, two fused operations
@@ -479,7 +677,18 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
             qbase = q_again ? sink + KP : qbase;
         }
         if (holds) {
-            if constexpr (BUF) {
+            if constexpr (COH != kCohOff) {
+                V* pr = reinterpret_cast<V*>(pbase + col);
+                V* qr = reinterpret_cast<V*>(qbase + col);
+                if (st.cp[j])
+                    st_coh<COH>(pr, np);
+                else
+                    *pr = np;
+                if (st.cq[j])
+                    st_coh<COH>(qr, nq);
+                else
+                    *qr = nq;
+            } else if constexpr (BUF) {
                 bp.template st<V>(np, cb, (uint32_t)u * kRowBytes);
                 bq.template st<V>(nq, cb, (uint32_t)v * kRowBytes);
             } else {

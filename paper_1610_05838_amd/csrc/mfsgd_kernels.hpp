@@ -13,11 +13,11 @@ constexpr int kHogwildBlock = 256; // 4 wavefronts per workgroup, each an indepe
 // wavefront w of the grid is worker w.  The XCDs' L2 caches are not coherent
 // with each other, so rows that several XCDs touch are updated in per-XCD
 // copies until evicted; the block-scheduled kernel below is the coherent form.
-template <int KP, typename T, int D, bool DBG, bool BUF = false>
+template <int KP, typename T, int D, bool DBG, bool BUF = false, int COH = kCohOff, bool ATOM = false>
 __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restrict__ S, int64_t nnz, int64_t W,
                                                            int f, T* __restrict__ P, T* __restrict__ Q, float lr,
                                                            float lp, float lq, DebugSink dbg, int sync_every,
-                                                           int sync_l1, int nx)
+                                                           int sync_l1, int nx, Coherence coh)
 {
     const int64_t worker = uniform64((int64_t)blockIdx.x * (kHogwildBlock / 64) + (threadIdx.x >> 6));
     if (worker >= W)
@@ -25,7 +25,7 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild(const Sample* __restr
     // workgroups are dealt to XCDs round-robin: the first wavefront of each of
     // the first nx workgroups leads its XCD's cache flushes
     const CacheSync sync{sync_every, (int)blockIdx.x < nx && (threadIdx.x >> 6) == 0, sync_l1 != 0};
-    run_worker<KP, T, D, DBG, false, BUF>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync);
+    run_worker<KP, T, D, DBG, false, BUF, COH, ATOM>(S, nnz, W, worker, f, P, Q, lr, lp, lq, dbg, sync, nullptr, coh);
 }
 
 // Row widths whose half-wavefront layout holds at most 16 bytes per lane.
@@ -99,14 +99,15 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // HALF (rows of 32 values, KP = 32): a wavefront claims two consecutive
 // batches of the block at once and runs them as two workers, one per half
 // (run_worker_half); the block's finished count advances by the batches run.
-template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false>
+template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false, bool ATOM = false>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, const int32_t* __restrict__ tmap,
                                                  const int32_t* __restrict__ xteams, int nx, int pool, int free_run,
                                                  uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
                                                  T* __restrict__ Q, float lr, float lp, float lq, int f,
                                                  uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
-                                                 DebugSink dbg, int32_t* trace, T* __restrict__ sink)
+                                                 DebugSink dbg, int32_t* trace, T* __restrict__ sink,
+                                                 Coherence coh)
 {
     static_assert(!HALF || (KP == 32 && !SKIP), "half-wavefront workers: rows of 32 values, no store redirection");
     constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per claim
@@ -226,8 +227,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
         if constexpr (HALF)
             run_worker_half<KP, T, D, DBG>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk);
         else
-            run_worker<KP, T, D, DBG, SKIP>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk, CacheSync{0, false, false},
-                                            my_sink);
+            run_worker<KP, T, D, DBG, SKIP, false, kCohOff, ATOM>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk,
+                                                                 CacheSync{0, false, false}, my_sink, coh);
         // this wavefront's stores have reached the XCD's L2 before it counts
         // the batches as finished
         __builtin_amdgcn_s_waitcnt(0);
@@ -562,43 +563,87 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
             }
         }
         const int64_t blocks = (a.W + 3) / 4;
+        const Coherence coh{a.hot_p, a.hot_q, a.coh_p != 0, a.coh_q != 0};
+        if constexpr (D == 1 && (sizeof(T) == 4 || Geo<KP>::E % 2 == 0)) {
+            if (a.atomic) {
+                // atomic row updates over the whole GPU; with coh == kCohBoth the
+                // rows are also read with agent-scope loads
+                if (a.coh == kCohBoth)
+                    hipLaunchKernelGGL((k_hogwild<KP, T, 1, DBG, false, kCohBoth, true>), dim3((unsigned)blocks),
+                                       dim3(kHogwildBlock), 0, st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg,
+                                       a.sync_every, a.sync_l1, a.nx, coh);
+                else
+                    hipLaunchKernelGGL((k_hogwild<KP, T, 1, DBG, false, kCohOff, true>), dim3((unsigned)blocks),
+                                       dim3(kHogwildBlock), 0, st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg,
+                                       a.sync_every, a.sync_l1, a.nx, coh);
+                return hipGetLastError();
+            }
+        }
+        if (a.atomic)
+            return hipErrorInvalidValue;
+        if (a.coh != kCohOff) {
+#define MFSGD_COH_LAUNCH(C)                                                                                        \
+    hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG, false, C>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st,   \
+                       a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx, coh)
+            switch (a.coh) {
+            case kCohStore: MFSGD_COH_LAUNCH(kCohStore); break;
+            case kCohBoth: MFSGD_COH_LAUNCH(kCohBoth); break;
+            case kCohNT: MFSGD_COH_LAUNCH(kCohNT); break;
+            case kCohSys: MFSGD_COH_LAUNCH(kCohSys); break;
+            default: return hipErrorInvalidValue;
+            }
+#undef MFSGD_COH_LAUNCH
+            return hipGetLastError();
+        }
         constexpr bool kDword = sizeof(T) * Geo<KP>::E == 4; // one dword of a row per lane
         if constexpr (kDword && !DBG) {
             if (a.buf) {
                 hipLaunchKernelGGL((k_hogwild<KP, T, D, false, true>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0,
                                    st, a.S, a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1,
-                                   a.nx);
+                                   a.nx, coh);
                 return hipGetLastError();
             }
         }
         hipLaunchKernelGGL((k_hogwild<KP, T, D, DBG>), dim3((unsigned)blocks), dim3(kHogwildBlock), 0, st, a.S,
-                           a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx);
+                           a.nnz, a.W, a.f, P, Q, a.lr, a.lp, a.lq, dbg, a.sync_every, a.sync_l1, a.nx, coh);
     } else if (a.scheme == kSchemeWaveLaunch) {
         const DebugSink dbg{a.visits, a.orig, nullptr};
         hipLaunchKernelGGL((k_wave<KP, T, D, DBG>), dim3((unsigned)a.s), dim3(64), 0, st, a.S, a.bstart, a.s, a.wave,
                            a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, dbg, a.trace_wave);
     } else {
         const DebugSink dbg{a.visits, a.orig, nullptr};
+        const Coherence acoh{a.hot_p, a.hot_q, false, false};
         if constexpr (KP == 32) {
             if (a.half && !a.sink) {
                 hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
                                    dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool,
                                    a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
-                                   a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr);
+                                   a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
             }
         }
+        if constexpr (D == 1 && (sizeof(T) == 4 || Geo<KP>::E % 2 == 0)) {
+            if (a.atomic) {
+                hipLaunchKernelGGL((k_blocked<KP, T, 1, DBG, false, false, true>), dim3((unsigned)a.grid),
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool,
+                                   a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
+                                   a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
+                return hipGetLastError();
+            }
+        }
+        if (a.atomic)
+            return hipErrorInvalidValue;
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
                                st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
-                               (T*)a.sink);
+                               (T*)a.sink, acoh);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
                                st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
-                               (T*)nullptr);
+                               (T*)nullptr, acoh);
     }
     return hipGetLastError();
 }

@@ -35,6 +35,11 @@ struct EpochLaunch {
     int nx;          // XCDs (one-address-space batch-Hogwild!: the first nx workgroups lead the flushes)
     int buf;         // every row offset of P and Q fits 31 bits: rows may be addressed through buffer descriptors
     int half;        // batch-Hogwild! at KP = 32: two workers per wavefront
+    int atomic;      // block-scheduled epochs at depth 1: rows updated with atomic adds
+    int coh;         // one-address-space batch-Hogwild!: coherence policy of rows that are not hot (kCoh*)
+    int coh_p, coh_q;                 // ... applied to P's / Q's rows
+    const uint32_t* hot_p;            // hot-row bits of P (nullptr: none)
+    const uint32_t* hot_q;            // hot-row bits of Q
     // block-scheduled epochs
     const int64_t* bstart;
     int s;           // grid side
@@ -128,6 +133,11 @@ struct PlanBuffers {
 // per-index sample counts for the balanced cut (indices out of range raise *bad)
 hipError_t plan_degrees(const Sample* S, int64_t nnz, int64_t m, int64_t n, unsigned long long* du,
                         unsigned long long* dv, int* bad, hipStream_t st);
+// *out = max(*out, deg[0 .. rows-1]) (the caller zeroes *out first)
+hipError_t max_degree(const unsigned long long* deg, int64_t rows, unsigned long long* out, hipStream_t st);
+// bits[i / 32] bit i % 32 = (deg[i] >= thr), for rows 0 .. rows-1 (the last word's spare bits clear)
+hipError_t hot_bits(const unsigned long long* deg, int64_t rows, unsigned long long thr, uint32_t* bits,
+                    hipStream_t st);
 // chunks of a plan: about one per kPlanChunkSamples samples, between
 // kPlanChunksMin and kPlanChunksMax, and at most kPlanCountBytes of counts
 constexpr int kPlanChunksMin = 2048;

@@ -54,6 +54,7 @@ def lib():
         sig = {
             "mfsgd_set_option": ([C.c_char_p, i64], C.c_int),
             "mfsgd_get_option": ([C.c_char_p, C.POINTER(i64)], C.c_int),
+            "mfsgd_reset_options": ([], C.c_int),
             "mfsgd_init": ([i64, i64, i32, u64], C.c_int),
             "mfsgd_plan": ([vp, i64, i32, vp], C.c_int),
             "mfsgd_epoch": ([vp, i64, f32, f32, f32, i32, vp], C.c_int),
@@ -116,6 +117,11 @@ def get_option(key: str) -> int:
     v = C.c_int64()
     _check(lib().mfsgd_get_option(key.encode(), C.byref(v)), "mfsgd_get_option")
     return v.value
+
+
+def reset_options() -> None:
+    """Every option back to its default."""
+    _check(lib().mfsgd_reset_options(), "mfsgd_reset_options")
 
 
 def init(m: int, n: int, k: int, seed: int) -> None:

@@ -34,28 +34,42 @@ def reset(M, **opts):
              sync_every=0, sync_l1=0, spin_limit=1 << 24, skip_stores=2, debug=0, wave_launch=0, half_waves=1, table_grid=256,
              table_workers=0)
     o.update(opts)
+    M.reset_options()
     for k, v in o.items():
         M.set_option(k, v)
 
 
-def test_bench_configuration_visits_every_sample_and_trains(M, netflix):
+def test_default_hogwild_visits_every_sample(M, netflix):
+    """The default batch-Hogwild! (one XCD, batches claimed in order) on the
+    full Netflix shape: every sample is used exactly once.  Its convergence
+    against the serial oracle is test_gpu_trajectory's."""
     import torch
     w, S, T, dS, dT = netflix
-    reset(M, debug=1)
+    reset(M, depth=0, debug=1)
     M.init(w["m"], w["n"], w["k"], w["seed"])
-    assert M.get_option("partitioned") == 0  # 255 MB of factors: one address space
-    r0 = M.rmse(dT)
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    assert M.get_option("hogwild_form") == 4  # the top item holds 9.6 % of the samples: one XCD
     v = M.debug_visits(len(S))
     assert bool(torch.all(v == 1)), "a sample was skipped or used twice"
-    M.set_option("debug", 0)
-    hist = [r0, M.rmse(dT)]
-    for t in range(1, 3):
-        M.epoch(dS, w["lr"] * w["decay"] ** t, w["lam"], w["lam"], "hogwild")
-        hist.append(M.rmse(dT))
-    print("test rmse by epoch", hist)
-    assert all(b < a for a, b in zip(hist, hist[1:]))
-    assert hist[-1] < 1.05  # the serial oracle reaches 0.939 after 3 epochs here
+
+
+def test_one_address_space_form_visits_every_sample(M, netflix):
+    """The one-address-space form over all XCDs (option partition = 0, not the
+    default: its per-XCD copies of the hot rows trail the serial order by more
+    than the Hogwild! tolerance on this shape): every sample used exactly once
+    and batch b run by worker b mod W."""
+    import torch
+    w, S, T, dS, dT = netflix
+    reset(M, partition=0, debug=3)
+    M.init(w["m"], w["n"], w["k"], w["seed"])
+    assert M.get_option("partitioned") == 0
+    M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    assert bool(torch.all(M.debug_visits(len(S)) == 1)), "a sample was skipped or used twice"
+    f = 256
+    nb = (len(S) + f - 1) // f
+    W = min(M.get_option("resident_waves"), nb)
+    tr = M.debug_trace(nb).cpu().numpy()
+    assert np.array_equal(tr, np.arange(nb) % W)
 
 
 def test_rmse_kernel_matches_oracle_on_trained_factors(M, netflix):
@@ -132,8 +146,8 @@ def test_half_wavefront_workers_at_full_size(M, netflix):
     """The Netflix shape trained at k = 32 (same samples): one address space
     with two workers per wavefront (every resident slot: 2 x resident
     wavefronts) uses every sample once with batch b on worker b mod W and
-    trains; the automatic (partitioned) form with paired claims uses every
-    sample once in the oracle's column orders."""
+    trains; the XCD-partitioned form with paired claims uses every sample
+    once in the oracle's column orders."""
     import torch
     w, S, T, dS, dT = netflix
     f = 256
@@ -153,9 +167,9 @@ def test_half_wavefront_workers_at_full_size(M, netflix):
         hist.append(M.rmse(dT))
     print("k = 32 half-wavefront test rmse by epoch", hist)
     assert all(b < a for a, b in zip(hist, hist[1:]))
-    reset(M, debug=3)
+    reset(M, partition=1, debug=3)
     M.init(w["m"], w["n"], 32, w["seed"])
-    assert M.get_option("partitioned") == 1  # 63.7 MB of factors
+    assert M.get_option("partitioned") == 1
     x = M.get_option("xcds")
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
     assert bool(torch.all(M.debug_visits(len(S)) == 1))

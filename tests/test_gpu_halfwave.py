@@ -43,6 +43,7 @@ def run(M, S, m, n, k, seed, dtype, epochs=1, **opts):
     o = dict(DEFAULTS)
     o["dtype"] = 1 if dtype == np.float16 else 0
     o.update(opts)
+    M.reset_options()
     for key, val in o.items():
         M.set_option(key, val)
     M.init(m, n, k, seed)
@@ -127,6 +128,7 @@ def test_schedule_and_coverage(M, k, W):
     S["u"] = rng.integers(0, m, nnz)
     S["v"] = rng.integers(0, n, nnz)
     S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
+    M.reset_options()
     for key, val in dict(DEFAULTS, debug=3, workers=W).items():
         M.set_option(key, val)
     M.init(m, n, k, seed)
@@ -166,6 +168,7 @@ def test_two_workers_rmse_gap(M, gen):
     S, T = gen.make(w)
     m, n, k, seed = w["m"], w["n"], w["k"], w["seed"]
     assert k <= 32
+    M.reset_options()
     for key, val in dict(DEFAULTS, workers=2).items():
         M.set_option(key, val)
     M.init(m, n, k, seed)
@@ -229,6 +232,7 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
     res = {}
     for half in (1, 0):
         o = dict(DEFAULTS, dtype=1 if dtype == np.float16 else 0, half_waves=half, **opts)
+        M.reset_options()
         for key, val in o.items():
             M.set_option(key, val)
         M.init(m, n, k, seed)
@@ -261,6 +265,7 @@ def test_block_scheduled_pairs_coverage_and_handover(M, gen, scheme, s, opts):
     block completed (claim and completion stamps of one event counter)."""
     w = gen.workload("netflix", m=30_000, n=4_000, ntrain=800_000, ntest=0)
     S = gen.draw(w, 0, w["ntrain"])
+    M.reset_options()
     for key, val in dict(DEFAULTS, **{"partition": 2, "debug": 3, "skip_stores": 0, **opts}).items():
         M.set_option(key, val)
     M.init(w["m"], w["n"], 32, w["seed"])
@@ -325,6 +330,7 @@ def test_wide_rows_schedule_and_coverage(M, dtype):
     S["v"] = rng.integers(0, n, nnz)
     S["r"] = rng.uniform(1.0, 5.0, nnz).astype(np.float32)
     for W in (7, 0):
+        M.reset_options()
         for key, val in dict(DEFAULTS, dtype=dtype, debug=3, workers=W, half_waves=2).items():
             M.set_option(key, val)
         M.init(m, n, 128, seed)
@@ -343,6 +349,7 @@ def test_half_workers_choice(M):
              (1, 1, 256, 0), (2, 0, 128, 1), (2, 0, 256, 0), (2, 1, 256, 1), (2, 1, 512, 0), (0, 0, 32, 0),
              (0, 1, 128, 0)]
     for half, dtype, k, want in cases:
+        M.reset_options()
         for key, val in dict(DEFAULTS, dtype=dtype, half_waves=half).items():
             M.set_option(key, val)
         M.init(50, 40, k, 1)

@@ -29,6 +29,7 @@ def setup(M, m, n, k, seed, dtype=np.float32, **opts):
     o = dict(DEFAULTS)
     o["dtype"] = 1 if dtype == np.float16 else 0
     o.update(opts)
+    M.reset_options()
     for key, val in o.items():
         M.set_option(key, val)
     M.init(m, n, k, seed)
