@@ -156,8 +156,8 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  as stay resident on the GPU (the automatic form: at most
  *                  min(m, n) / 20, see MFSGD_BATCH_HOGWILD).
  *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8, or
- *                  0 (default) automatically: 1 for the automatic and
- *                  one-XCD batch-Hogwild! forms (bound by bandwidth, not
+ *                  0 (default) automatically: 1 for the one-XCD
+ *                  batch-Hogwild! form (the automatic form always runs 1) (bound by bandwidth, not
  *                  latency, so one in flight runs as fast and halves the
  *                  updates in flight), 2 elsewhere.  A wavefront forwards
  *                  its own pending updates, so depth never changes the
@@ -385,8 +385,11 @@ int64_t mfsgd_get_epoch(void);
  *                      made while debug bit 0 was set).
  *   MFSGD_DBG_TEAM_MAP : the team layout of the last block-scheduled epoch:
  *                      count = its workgroup count (read-only option
- *                      "teams_grid"), dst int32 -- team << 16 | member of
- *                      each workgroup, -1 for an idle one.
+ *                      "teams_grid"), dst int32 -- team << 16 | member, -1
+ *                      for an idle slot.  Teams of several wavefronts: entry
+ *                      x * (count / xcds) + j is the j-th workgroup to start
+ *                      on XCD x (each workgroup reads its XCD from the
+ *                      hardware); one-wavefront teams: entry b is workgroup b.
  *   MFSGD_DBG_TEAM_SIZES : same layout, count = s, dst int32 -- workgroups
  *                      of each team.
  *   MFSGD_DBG_TABLE_STARTS : the global-table plan: count = s*s+1 (s =

@@ -171,7 +171,7 @@ struct Context {
     const Plan* lay_plan = nullptr;
     uint64_t lay_version = 0;
     int64_t lay_want = -1;
-    int lay_grid = 0, lay_waves = 0, lay_depth = 0, lay_half = -1;
+    int lay_grid = 0, lay_waves = 0, lay_depth = 0, lay_half = -1, lay_xslots = 0;
 };
 
 Options g_opt;
@@ -546,10 +546,14 @@ int detect_xcds(Context& c)
     dfree(dev);
     if (e != hipSuccess)
         return fail(MFSGD_EHIP, std::string("XCD probe: ") + hipGetErrorString(e));
+    // the number of XCDs: distinct ids among 64 one-wavefront workgroups,
+    // which the dispatcher deals round-robin (starting wherever the previous
+    // launch left off); the block-scheduled kernel reads each workgroup's XCD
+    // itself, so only the count matters here
     const int nx = 1 + *std::max_element(host.begin(), host.end());
-    bool round_robin = nx >= 1 && nx <= kMaxGrid;
+    bool round_robin = nx >= 1 && nx <= kMaxGrid && host[0] >= 0;
     for (int b = 0; round_robin && b < kProbe; ++b)
-        round_robin = host[b] == b % nx;
+        round_robin = host[b] == (host[0] + b) % nx;
     c.nx = round_robin ? nx : 1;
     return MFSGD_OK;
 }
@@ -1004,6 +1008,7 @@ struct TeamLayout {
     std::vector<int32_t> tmap, tsize;
     std::vector<int32_t> xteams; // per XCD: team count, then the teams placed there
     int64_t grid = 0;
+    int64_t xslots = 0; // pooled: workgroup slots per XCD (0: one-wavefront teams, mapped by workgroup)
 };
 
 int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, int64_t uniform, TeamLayout& L)
@@ -1064,17 +1069,22 @@ int build_team_layout(const std::vector<int64_t>& load, int nx, int64_t slots, i
         int32_t* xt = &L.xteams[(size_t)xcd[t] * (kMaxGrid + 1)];
         xt[1 + xt[0]++] = t;
     }
+    // tmap[x * rows + j]: the team of the j-th workgroup that starts on XCD x
+    // (the kernel reads its XCD from the hardware and counts arrivals); the
+    // grid holds rows workgroups per XCD, which the dispatcher deals out
+    // round-robin, and any surplus on one XCD leaves at once
     std::vector<int64_t> fill(nx, 0);
     for (int t = 0; t < s; ++t)
         fill[xcd[t]] += L.tsize[t];
     const int64_t rows = *std::max_element(fill.begin(), fill.end());
     L.grid = rows * nx;
+    L.xslots = rows;
     L.tmap.assign((size_t)L.grid, -1);
     std::fill(fill.begin(), fill.end(), 0);
     for (int t = 0; t < s; ++t)
         for (int m = 0; m < L.tsize[t]; ++m) {
             const int x = xcd[t];
-            L.tmap[(size_t)(fill[x] * nx + x)] = (t << 16) | m;
+            L.tmap[(size_t)(x * rows + fill[x])] = (t << 16) | m;
             fill[x] += 1;
         }
     return MFSGD_OK;
@@ -1145,8 +1155,10 @@ int team_layout(const Plan& pl, int64_t want, bool half, EpochLaunch& a)
         c.lay_depth = a.depth;
         c.lay_half = (int)half;
         c.lay_grid = (int)L.grid;
+        c.lay_xslots = (int)L.xslots;
     }
     a.grid = c.lay_grid;
+    a.xslots = c.lay_xslots;
     a.tmap = c.tmap;
     a.xteams = c.xteams;
     a.nx = nx;
@@ -1206,7 +1218,8 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
 
     EpochLaunch a{};
     a.KP = c.KP;
-    a.depth = depth_for(hog && (form == 4 || atomic));
+    // the automatic form always runs one sample in flight (atomic adds need it)
+    a.depth = automatic ? 1 : depth_for(hog && (form == 4 || atomic));
     a.nnz = nnz;
     a.f = (int)g_opt.batch_f;
     a.P = c.P;

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // (run_worker_half); the block's finished count advances by the batches run.
 template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false, bool ATOM = false>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
-                                                 int s, const int32_t* __restrict__ tmap,
+                                                 int s, int xslots, const int32_t* __restrict__ tmap,
                                                  const int32_t* __restrict__ xteams, int nx, int pool, int free_run,
                                                  uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
                                                  T* __restrict__ Q, float lr, float lp, float lq, int f,
@@ -112,7 +112,29 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     static_assert(!HALF || (KP == 32 && !SKIP), "half-wavefront workers: rows of 32 values, no store redirection");
     constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per claim
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
-    const int tm = tmap[blockIdx.x];
+    __shared__ int s_tm, s_x;
+    uint32_t* const arrived = sched + 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1;
+    if (threadIdx.x == 0) {
+        if (xslots > 0) {
+            // pooled teams: the XCD this workgroup runs on (hardware register)
+            // and its arrival order there select its team, so a team's
+            // wavefronts share one L2 whatever order the dispatcher uses
+            unsigned xcc;
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+            const int x = (int)(xcc & 0xfu) % nx;
+            const uint32_t slot =
+                __hip_atomic_fetch_add(arrived + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_x = x;
+            s_tm = slot < (uint32_t)xslots ? tmap[(int64_t)x * xslots + slot] : -1;
+        } else {
+            s_x = 0;
+            s_tm = tmap[blockIdx.x];
+        }
+        shuffle_perm(sigma_c, s, Cperm);
+        shuffle_perm(sigma_o, s, Ooff);
+    }
+    __syncthreads();
+    const int tm = s_tm;
     if (tm < 0)
         return;
     const int home = tm >> 16;
@@ -126,15 +148,10 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     uint32_t* const stamps = trace ? reinterpret_cast<uint32_t*>(trace) + (int64_t)s * s : nullptr;
     // two private rows per wavefront of the grid for skipped stores
     T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
-    if (threadIdx.x == 0) {
-        shuffle_perm(sigma_c, s, Cperm);
-        shuffle_perm(sigma_o, s, Ooff);
-    }
-    __syncthreads();
 
     // lane j < nt watches the j-th team of this wavefront's preference order:
     // the home team, then the other teams of the XCD in list order
-    const int32_t* xt = xteams + (int64_t)(blockIdx.x % nx) * (kMaxGrid + 1);
+    const int32_t* xt = xteams + (int64_t)s_x * (kMaxGrid + 1);
     const int nt = pool ? xt[0] : 1;
     int hidx = 0;
     for (int j = 0; pool && j < nt; ++j)
@@ -616,7 +633,7 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (KP == 32) {
             if (a.half && !a.sink) {
                 hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool,
                                    a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
@@ -625,7 +642,7 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (D == 1 && (sizeof(T) == 4 || Geo<KP>::E % 2 == 0)) {
             if (a.atomic) {
                 hipLaunchKernelGGL((k_blocked<KP, T, 1, DBG, false, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool,
                                    a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
@@ -636,12 +653,12 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)a.sink, acoh);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)nullptr, acoh);
     }

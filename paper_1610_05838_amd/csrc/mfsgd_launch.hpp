@@ -14,8 +14,9 @@ constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never ch
 constexpr int kSchemeHogwild = 0;
 constexpr int kSchemeWavefront = 1;
 constexpr int kSchemeWaveLaunch = 2; // one deterministic wavefront-update wave per launch (cross-check)
-// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team, event counter
-constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1;
+// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team, event counter,
+// workgroups arrived per XCD
+constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1 + kMaxGrid;
 
 struct DebugSink;
 
@@ -44,7 +45,9 @@ struct EpochLaunch {
     const int64_t* bstart;
     int s;           // grid side
     int grid;        // workgroups launched
-    const int32_t* tmap;   // per workgroup: home team << 16 | member, or -1 (idle)
+    int xslots;      // pooled teams: workgroup slots per XCD (tmap rows), 0: one-wavefront teams
+    const int32_t* tmap;   // pooled: per (XCD, arrival slot) home team << 16 | member, or -1 (idle);
+                           // one-wavefront teams: per workgroup
     const int32_t* xteams; // per XCD x: [x * (kMaxGrid + 1)] = team count, then the teams placed on x
     int pool;              // 1: a wavefront also serves the other teams of its XCD
     int free_run;          // 1: blocks open without waiting for their column ticket

@@ -243,8 +243,9 @@ def debug_table_order(nnz: int, stream=None) -> torch.Tensor:
 
 
 def debug_team_layout(s: int, stream=None):
-    """(map, sizes) of the last block-scheduled epoch: per workgroup
-    team << 16 | member (-1 idle), per team its workgroup count."""
+    """(map, sizes) of the last block-scheduled epoch: per (XCD x, arrival
+    slot j) at x * (len(map) / xcds) + j -- or per workgroup for one-wavefront
+    teams -- team << 16 | member (-1 idle), per team its workgroup count."""
     grid = get_option("teams_grid")
     tmap = torch.empty(max(grid, 1), dtype=torch.int32, device="cuda")
     sizes = torch.empty(s, dtype=torch.int32, device="cuda")

@@ -170,9 +170,10 @@ def test_yahoo_shape_full_size(M, gen):
     T = gen.draw(w, w["ntrain"], w["ntest"])
     dT = M.samples_to_device(T)
     setup(M, w, debug=1)
-    assert M.get_option("partitioned") == 1  # 832 MB of factors, beyond the Infinity Cache: partitioned
     hist = [M.rmse(dT)]
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "hogwild")
+    # no row holds 1/64 of the samples: one address space, atomic adds
+    assert M.get_option("hogwild_form") == 0 and M.get_option("hogwild_atomic") == 1
     assert bool(torch.all(M.debug_visits(w["ntrain"]) == 1))
     M.set_option("debug", 0)
     hist.append(M.rmse(dT))

@@ -227,11 +227,12 @@ def test_team_layout_follows_row_loads(M, s):
     load = starts[s::s] - starts[:-1:s]
     xcd = {}
     members = {t: [] for t in range(s)}
+    rows = len(tmap) // nx  # entry x * rows + j: the j-th workgroup to start on XCD x
     for b, e in enumerate(tmap):
         if e < 0:
             continue
         t, mem = int(e) >> 16, int(e) & 0xFFFF
-        assert xcd.setdefault(t, b % nx) == b % nx
+        assert xcd.setdefault(t, b // rows) == b // rows
         members[t].append(mem)
     for t in range(s):
         assert sorted(members[t]) == list(range(sizes[t])) and sizes[t] >= 1
