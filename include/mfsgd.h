@@ -336,6 +336,24 @@ int mfsgd_epoch_staged(const mfsgd_sample* samples, int64_t nnz, float lr, float
  * ENUMERIC: the result is not finite (it is still written). */
 int mfsgd_rmse(const mfsgd_sample* test, int64_t ntest, double* rmse_out, void* stream);
 
+/* The same test RMSE for callers that cannot allocate or synchronise: code
+ * under HIP graph capture and tight serving loops.  Enqueues the two RMSE
+ * kernels on `stream` and returns at once; the result (0 for ntest == 0) is
+ * written to *rmse_dev, one binary64 in caller-owned DEVICE memory, when the
+ * stream reaches it.  Same kernels and summation order as mfsgd_rmse, hence
+ * the same value bit for bit.  It calls no allocation routine: the 2048
+ * partial sums go to a fixed 16 KiB array in device memory (one per GPU,
+ * held until the process ends; its address is taken at mfsgd_init on the
+ * device current then), which every call on that GPU reuses and fully
+ * rewrites -- calls that overlap on one GPU (two streams, or two threads)
+ * race on it.  ntest is not limited by the scratch (the partial count is
+ * fixed).  Errors: ESTATE before mfsgd_init or when the current device is
+ * not the one mfsgd_init ran on; EINVAL for a bad array or NULL rmse_dev;
+ * EHIP for a launch failure.  Device-side errors and a non-finite result
+ * are not reported here (nothing is waited for): mfsgd_sync reports the
+ * former, the caller checks the value. */
+int mfsgd_rmse_noalloc(const mfsgd_sample* test, int64_t ntest, double* rmse_dev, void* stream);
+
 /* Check that every sample index is in range.  Synchronises `stream`.
  * EINVAL if any is not. */
 int mfsgd_check_samples(const mfsgd_sample* samples, int64_t nnz, void* stream);

@@ -12,10 +12,20 @@
 #include "mfsgd_device.hpp"
 #include "mfsgd_launch.hpp"
 
+// Scratch of mfsgd_rmse_noalloc: the kRmseWaves binary64 partial sums of the
+// RMSE's first pass, in a fixed device array so that the call allocates
+// nothing.  In host code `rmse_scratch` names a host-side stand-in; its device
+// address, one per GPU, comes from hipGetSymbolAddress at mfsgd_init.
+constexpr int kRmseScratchDoubles = 2048;
+static __device__ __align__(256) double rmse_scratch[kRmseScratchDoubles];
+
 namespace {
 
 using namespace mfsgd;
 
+static_assert(kRmseWaves <= kRmseScratchDoubles, "the RMSE partial sums must fit the no-alloc scratch");
+constexpr int kMaxDevices = 64;
+double* g_rmse_scratch[kMaxDevices] = {}; // device address of rmse_scratch per GPU
 
 thread_local std::string g_err;
 
@@ -570,6 +580,11 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     c.last_atomic = 0;
     c.stats = RowStats();
     HIPCHK(hipGetDevice(&c.device));
+    if (c.device >= 0 && c.device < kMaxDevices && !g_rmse_scratch[c.device]) {
+        void* sp = nullptr;
+        HIPCHK(hipGetSymbolAddress(&sp, HIP_SYMBOL(rmse_scratch)));
+        g_rmse_scratch[c.device] = (double*)sp;
+    }
     HIPCHK(hipDeviceGetAttribute(&c.cus, hipDeviceAttributeMultiprocessorCount, c.device));
     c.m = m;
     c.n = n;
@@ -1550,6 +1565,33 @@ int rmse_impl(const mfsgd_sample* test, int64_t ntest, double* out, hipStream_t 
     return MFSGD_OK;
 }
 
+// RMSE into a caller-owned device double, asynchronously, with the partial
+// sums in the device's rmse_scratch array: no allocation, no host copy, no
+// synchronisation (so it can be captured in a HIP graph).
+int rmse_noalloc_impl(const mfsgd_sample* test, int64_t ntest, double* out, hipStream_t st)
+{
+    Context& c = g;
+    if (!c.inited)
+        return fail(MFSGD_ESTATE, "mfsgd_init has not been called");
+    if (!valid_samples(test, ntest) || !out)
+        return fail(MFSGD_EINVAL, "bad test array or NULL output");
+    int dev = -1;
+    HIPCHK(hipGetDevice(&dev));
+    if (dev != c.device)
+        return fail(MFSGD_ESTATE, "the current device is not the one mfsgd_init ran on");
+    if (dev < 0 || dev >= kMaxDevices || !g_rmse_scratch[dev])
+        return fail(MFSGD_ESTATE, "no RMSE scratch address for this device");
+    double* scr = g_rmse_scratch[dev];
+    if (ntest > 0) {
+        if (c.dtype == MFSGD_FP16)
+            HIPCHK(rmse_partial_f16(c.KP, (const Sample*)test, ntest, c.P, c.Q, scr, st));
+        else
+            HIPCHK(rmse_partial_f32(c.KP, (const Sample*)test, ntest, c.P, c.Q, scr, st));
+    }
+    HIPCHK(rmse_final(scr, ntest, out, st));
+    return MFSGD_OK;
+}
+
 int factors_impl(void* P, void* Q, const void* Pin, const void* Qin, hipStream_t st)
 {
     Context& c = g;
@@ -1667,6 +1709,11 @@ int mfsgd_epoch_staged(const mfsgd_sample* samples, int64_t nnz, float lr, float
 int mfsgd_rmse(const mfsgd_sample* test, int64_t ntest, double* rmse_out, void* stream)
 {
     return guarded([&]() -> int { return rmse_impl(test, ntest, rmse_out, (hipStream_t)stream); });
+}
+
+int mfsgd_rmse_noalloc(const mfsgd_sample* test, int64_t ntest, double* rmse_dev, void* stream)
+{
+    return guarded([&]() -> int { return rmse_noalloc_impl(test, ntest, rmse_dev, (hipStream_t)stream); });
 }
 
 int mfsgd_check_samples(const mfsgd_sample* samples, int64_t nnz, void* stream)

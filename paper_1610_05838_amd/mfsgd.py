@@ -60,6 +60,7 @@ def lib():
             "mfsgd_epoch": ([vp, i64, f32, f32, f32, i32, vp], C.c_int),
             "mfsgd_epoch_staged": ([vp, i64, f32, f32, f32, vp], C.c_int),
             "mfsgd_rmse": ([vp, i64, C.POINTER(C.c_double), vp], C.c_int),
+            "mfsgd_rmse_noalloc": ([vp, i64, vp, vp], C.c_int),
             "mfsgd_check_samples": ([vp, i64, vp], C.c_int),
             "mfsgd_sync": ([vp], C.c_int),
             "mfsgd_get_factors": ([vp, vp, vp], C.c_int),
@@ -161,6 +162,15 @@ def rmse(test: torch.Tensor, stream=None) -> float:
     out = C.c_double()
     _check(lib().mfsgd_rmse(p, n, C.byref(out), _stream(stream)), "mfsgd_rmse")
     return out.value
+
+
+def rmse_noalloc(test: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """Enqueue the test RMSE into out[0] (a float64 device tensor) without
+    allocating or waiting (mfsgd_rmse_noalloc)."""
+    if out.dtype != torch.float64 or not out.is_cuda or out.numel() < 1:
+        raise ValueError("out must be a float64 device tensor with at least one element")
+    p, n = _samples_ptr(test)
+    _check(lib().mfsgd_rmse_noalloc(p, n, C.c_void_p(out.data_ptr()), _stream(stream)), "mfsgd_rmse_noalloc")
 
 
 def check_samples(samples: torch.Tensor, stream=None) -> None:
