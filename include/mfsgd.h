@@ -170,6 +170,15 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  worker on one XCD, the XCDs loaded as evenly as the row
  *                  blocks allow).  A worker's wavefronts prefer its blocks
  *                  but also serve the other workers on their XCD.
+ *   "priority"     pooled block-scheduled epochs: 1 (default) a wavefront
+ *                  that finds several open blocks takes the one whose
+ *                  column block holds the most samples among the columns
+ *                  holding over 1.5 times the mean (such a column's chain of
+ *                  blocks bounds the epoch); otherwise, and with 0, its own
+ *                  worker's block first.
+ *   "tail_claims"  pooled block-scheduled epochs: 1 claims a block's last
+ *                  2 units of 64 samples per wavefront of the XCD one unit
+ *                  at a time instead of in batches of f; 0 (default).
  *   "partition"    batch-Hogwild! form, 0 to 4 (default 2, automatic; see
  *                  MFSGD_BATCH_HOGWILD).
  *   "atomic"       1: batch-Hogwild! in one address space or in one XCD adds
@@ -251,8 +260,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  sample; a block-scheduled epoch needs a plan made while
  *                  bit 0 was set.
  * Read-only keys (after mfsgd_init): "resident_waves" (wavefronts of the
- * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs the
- * workgroups are dealt to, 1 if the dealing is not round-robin), "cus",
+ * one-address-space epoch kernel the GPU holds at once), "xcds" (XCDs: the
+ * largest hardware XCD id an init probe saw, plus one), "xcd_round_robin" (1
+ * if that probe's workgroups were dealt round-robin), "cus",
  * "partitioned" (whether batch-Hogwild! runs block-scheduled: the last
  * epoch's form, or before one the option's), "hogwild_form" (form of the last
  * batch-Hogwild! epoch, values of "partition" other than 2; -1 before one),
@@ -388,7 +398,11 @@ int64_t mfsgd_get_epoch(void);
  *                      a batch of that block, the next entry = the completion
  *                      of its last batch (the block of wave w+1 in the same
  *                      column is claimed only after that; 0xffffffff where
- *                      not recorded, e.g. per-wave launches);
+ *                      not recorded, e.g. per-wave launches), optionally
+ *                      followed by 2*s*s clock stamps (count up to 5*s*s):
+ *                      the low 32 bits of the 100 MHz realtime counter when
+ *                      the block's first batch was claimed and when its last
+ *                      batch completed, same order;
  *                      global table: dst int32[3*B], B = "table_blocks": for
  *                      decision d, entry 3d = the block id I*s+J taken, 3d+1
  *                      and 3d+2 = the values of one event counter when the

@@ -48,6 +48,8 @@ struct Options {
     int64_t table_grid = 256;
     int64_t table_workers = 0;
     int64_t atomic = 0;
+    int64_t priority = 1;
+    int64_t tail_claims = 0;
     int64_t coherent = 0;
     int64_t coherent_mat = 3;
     int64_t hot_log2 = 0;
@@ -82,6 +84,7 @@ struct Plan {
     int64_t orig_cap = 0;
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
+    uint32_t* colw = nullptr;    // kMaxGrid: priority weight of each column block (0: none)
     double hot_col = 0.0;        // largest share of a column block's samples held by one item
     double hot_row = 0.0;        // largest share of a row block's samples held by one user
     uint64_t version = 0;        // bumped by every build
@@ -128,7 +131,8 @@ struct Context {
     bool inited = false;
     int device = 0;
     int cus = 0;
-    int nx = 1; // XCDs workgroups are dealt to round-robin (1 if not that layout)
+    int nx = 1;      // XCDs: distinct hardware XCD ids the init probe saw
+    bool rr = false; // the probe's workgroups were dealt round-robin (b on XCD (b + o) mod nx)
     int64_t m = 0, n = 0;
     int k = 0, KP = 0, dtype = 0;
     uint64_t seed = 0;
@@ -257,6 +261,7 @@ int grow(T** p, int64_t* cap, int64_t need, const char* what)
 
 void free_plan(Plan& p)
 {
+    dfree(p.colw);
     dfree(p.Sp);
     dfree(p.orig);
     dfree(p.bstart);
@@ -472,6 +477,8 @@ const OptSpec kOpts[] = {
     {"table_grid", &Options::table_grid, 1, kMaxTableGrid, "table_grid must be in [1, 1024]"},
     {"table_workers", &Options::table_workers, 0, 65536, "table_workers must be in [0, 65536]"},
     {"atomic", &Options::atomic, 0, 1, "atomic must be 0 or 1"},
+    {"priority", &Options::priority, 0, 1, "priority must be 0 or 1"},
+    {"tail_claims", &Options::tail_claims, 0, 1, "tail_claims must be 0 or 1"},
     {"coherent", &Options::coherent, 0, 4, "coherent must be in [0, 4]"},
     {"coherent_mat", &Options::coherent_mat, 0, 3, "coherent_mat must be in [0, 3]"},
     {"hot_log2", &Options::hot_log2, 0, 62, "hot_log2 must be in [0, 62]"},
@@ -511,7 +518,7 @@ int get_option_impl(const char* key, int64_t* value)
                     !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
                     !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks") ||
                     !std::strcmp(key, "half_workers") || !std::strcmp(key, "hogwild_form") ||
-                    !std::strcmp(key, "hogwild_atomic");
+                    !std::strcmp(key, "hogwild_atomic") || !std::strcmp(key, "xcd_round_robin");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
@@ -520,6 +527,8 @@ int get_option_impl(const char* key, int64_t* value)
         *value = (int64_t)g.cus * occupancy_waves(g.KP, g.dtype, depth_for(false));
     else if (!std::strcmp(key, "xcds"))
         *value = g.nx;
+    else if (!std::strcmp(key, "xcd_round_robin"))
+        *value = g.rr ? 1 : 0;
     else if (!std::strcmp(key, "half_workers"))
         *value = half_wave_workers(g.KP, g.dtype) ? 1 : 0;
     else if (!std::strcmp(key, "blocked_per_cu"))
@@ -556,15 +565,21 @@ int detect_xcds(Context& c)
     dfree(dev);
     if (e != hipSuccess)
         return fail(MFSGD_EHIP, std::string("XCD probe: ") + hipGetErrorString(e));
-    // the number of XCDs: distinct ids among 64 one-wavefront workgroups,
-    // which the dispatcher deals round-robin (starting wherever the previous
-    // launch left off); the block-scheduled kernel reads each workgroup's XCD
-    // itself, so only the count matters here
-    const int nx = 1 + *std::max_element(host.begin(), host.end());
-    bool round_robin = nx >= 1 && nx <= kMaxGrid && host[0] >= 0;
+    // the number of XCDs: the largest id among 64 one-wavefront workgroups
+    // plus one.  The block-scheduled kernel reads each workgroup's XCD from
+    // the hardware itself, so it needs only this count, whatever order the
+    // dispatcher deals the workgroups in; whether that order was round-robin
+    // (starting wherever the previous launch left off) is kept for the
+    // epoch kernel's optional periodic cache flushes, led by the first nx
+    // workgroups of its grid.
+    const int top = *std::max_element(host.begin(), host.end());
+    if (*std::min_element(host.begin(), host.end()) < 0 || top >= kMaxGrid)
+        return fail(MFSGD_EHIP, "XCD probe: unexpected XCD id");
+    c.nx = top + 1;
+    bool round_robin = true;
     for (int b = 0; round_robin && b < kProbe; ++b)
-        round_robin = host[b] == (host[0] + b) % nx;
-    c.nx = round_robin ? nx : 1;
+        round_robin = host[b] == (host[0] + b) % c.nx;
+    c.rr = round_robin;
     return MFSGD_OK;
 }
 
@@ -757,6 +772,8 @@ int build_hot(const mfsgd_sample* samples, int64_t nnz, int log2, hipStream_t st
     return MFSGD_OK;
 }
 
+constexpr double kCriticalRatio = 1.5;
+
 int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool balanced, bool keep_orig,
                hipStream_t st)
 {
@@ -837,6 +854,25 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     HIPCHK(hipMemcpyAsync(pl.hstart.data(), pl.bstart, sizeof(int64_t) * pl.hstart.size(), hipMemcpyDeviceToHost,
                           st));
     HIPCHK(hipStreamSynchronize(st));
+    // Column priorities for pooled wavefronts: a column block holding well
+    // over its share of the samples is worked by one team after another for
+    // the whole epoch (its chain of blocks bounds the epoch), so a wavefront
+    // that finds several open blocks takes the one in the heaviest such
+    // column.  Columns within kCriticalRatio of the mean get no priority.
+    {
+        std::vector<uint32_t> w(kMaxGrid, 0u);
+        std::vector<int64_t> col(s, 0);
+        for (int t = 0; t < s; ++t)
+            for (int j = 0; j < s; ++j)
+                col[j] += pl.hstart[(size_t)t * s + j + 1] - pl.hstart[(size_t)t * s + j];
+        const double mean = (double)nnz / (double)s;
+        for (int j = 0; j < s; ++j)
+            if ((double)col[j] > kCriticalRatio * mean)
+                w[j] = (uint32_t)std::min<int64_t>(col[j] / 64 + 1, 0xffffffffll);
+        if (!pl.colw)
+            CHK(dalloc((void**)&pl.colw, sizeof(uint32_t) * kMaxGrid, "column priorities"));
+        HIPCHK(hipMemcpy(pl.colw, w.data(), sizeof(uint32_t) * kMaxGrid, hipMemcpyHostToDevice));
+    }
     pl.version += 1;
     pl.src = samples;
     pl.nnz = nnz;
@@ -1018,7 +1054,8 @@ int check_impl(const mfsgd_sample* samples, int64_t nnz, hipStream_t st)
 // fewest samples so far; then each XCD's workgroup slots are shared among its
 // teams: one each, the rest in proportion to the samples of the team's row
 // block (largest remainders first), or `uniform` per team if uniform > 0.
-// Slot j of XCD x is workgroup j * nx + x (round-robin dispatch).
+// Slot j of XCD x is the j-th workgroup that starts on XCD x (the kernel
+// reads its XCD from the hardware and counts arrivals).
 struct TeamLayout {
     std::vector<int32_t> tmap, tsize;
     std::vector<int32_t> xteams; // per XCD: team count, then the teams placed there
@@ -1180,6 +1217,9 @@ int team_layout(const Plan& pl, int64_t want, bool half, EpochLaunch& a)
     a.pool = want == 1 ? 0 : 1;
     a.wg_waves = waves;
     a.sink = skip_stores(pl) ? c.sink : nullptr;
+    a.colw = g_opt.priority && a.pool ? pl.colw : nullptr;
+    // the last 2 units per wavefront of the XCD go one unit per claim
+    a.tail = a.pool && g_opt.tail_claims ? (uint32_t)std::min<int64_t>(2 * (int64_t)c.lay_xslots * waves, 1 << 30) : 0u;
     a.half = 0;
     return MFSGD_OK;
 }
@@ -1365,8 +1405,8 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.free_run = hog && form == 3 ? 1 : 0;
         a.orig = (dbg & 1) ? pl->orig : nullptr;
         if (dbg & 2) {
-            // columns, then two event stamps per (team, wave)
-            const int64_t words = 3 * (int64_t)s * s;
+            // columns, then two event stamps and two clock stamps per (team, wave)
+            const int64_t words = 5 * (int64_t)s * s;
             CHK(grow(&c.trace, &c.trace_cap, words, "trace"));
             c.trace_n = words;
             HIPCHK(hipMemsetAsync(c.trace, 0xff, sizeof(int32_t) * (size_t)words, st));

@@ -165,6 +165,19 @@ __device__ __forceinline__ float wave_sum(float x)
 
 __device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
 
+// Agent-scope release that has finished before the next store issues: the
+// fence writes this XCD's L2 back (buffer_wbl2), and the write-back counts on
+// the vector memory counter like a store.  The fence's own wait for it is
+// left out by this compiler's wait-count pass whenever no other memory
+// operation is outstanding (it does not count the write-back), so a flag
+// stored next could reach another XCD before the rows it publishes; the
+// explicit wait keeps the order.
+__device__ __forceinline__ void release_agent()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_s_waitcnt(0);
+}
+
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ int64_t uniform64(int64_t x)
@@ -725,7 +738,7 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
         }
         if (sync.every > 0 && c_off == 0 && ++batches % sync.every == 0) {
             if (sync.leader) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                release_agent();
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             } else if (sync.l1) {
                 asm volatile("buffer_inv sc0" ::: "memory");
@@ -963,7 +976,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
         }
         if (sync.every > 0 && c_off == 0 && ++batches % sync.every == 0) {
             if (sync.leader) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                release_agent();
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             } else if (sync.l1) {
                 asm volatile("buffer_inv sc0" ::: "memory");

@@ -65,8 +65,9 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // the team's row block).  cursor[t] is the lowest wave of team t that may still
 // have unclaimed batches.
 //
-// Every team lives on one XCD (workgroup b runs on XCD b mod nx, checked at
-// init), so all updates of a team meet in that XCD's L2.  In pool mode a
+// Every team lives on one XCD (pooled teams: a workgroup reads its XCD from
+// the hardware and joins a team placed there; one-wavefront teams are single
+// wavefronts), so all updates of a team meet in that XCD's L2.  In pool mode a
 // wavefront serves its home team first and otherwise any open block of the
 // other teams on its XCD; without pool mode (one-wavefront teams: the
 // deterministic schedule) only its home team.  Rows move between XCDs only
@@ -85,9 +86,18 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // A wait for an open block that exceeds spin_limit polls raises *err; every
 // wavefront that then finds nothing to claim leaves, so the grid drains.
 //
-// sched: [0, G2) batches finished per (team, wave), [G2, 2 G2) next batch to
-// claim per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, then one
-// event counter, where G2 = kMaxGrid^2; all zero at launch.
+// Claims are counted in units of 64 samples: a block's first units go in
+// head claims of f samples (2 f with HALF), its last `tail` units one at a
+// time, so that the block ends with many wavefronts finishing small pieces.
+// Among the open blocks a wavefront can serve, it takes the first in its
+// preference order (home team first) unless colw gives another one's
+// column a higher weight (a column holding well over its share of the
+// samples is a chain of blocks that bounds the epoch).
+//
+// sched: [0, G2) units finished per (team, wave), [G2, 2 G2) head claims
+// taken per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, one event
+// counter, kMaxGrid workgroups arrived per XCD, then [.., + G2) unit claims
+// taken per (team, wave), where G2 = kMaxGrid^2; all zero at launch.
 //
 // Debug (trace != nullptr): trace[t*s + w] = column of team t in wave w, and
 // after those s*s entries two stamps per (team, wave) from the event counter:
@@ -99,18 +109,21 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // HALF (rows of 32 values, KP = 32): a wavefront claims two consecutive
 // batches of the block at once and runs them as two workers, one per half
 // (run_worker_half); the block's finished count advances by the batches run.
+
 template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false, bool ATOM = false>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, int xslots, const int32_t* __restrict__ tmap,
-                                                 const int32_t* __restrict__ xteams, int nx, int pool, int free_run,
-                                                 uint64_t sigma_c, uint64_t sigma_o, T* __restrict__ P,
+                                                 const int32_t* __restrict__ xteams, int nx, int pool,
+                                                 const uint32_t* __restrict__ colw, int free_run,
+                                                 uint64_t sigma_c, uint64_t sigma_o, uint32_t tail, T* __restrict__ P,
                                                  T* __restrict__ Q, float lr, float lp, float lq, int f,
                                                  uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
                                                  DebugSink dbg, int32_t* trace, T* __restrict__ sink,
                                                  Coherence coh)
 {
     static_assert(!HALF || (KP == 32 && !SKIP), "half-wavefront workers: rows of 32 values, no store redirection");
-    constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per claim
+    constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per head claim
+    constexpr uint32_t kUnit = 64;              // samples per claim unit
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
     __shared__ int s_tm, s_x;
     uint32_t* const arrived = sched + 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1;
@@ -145,7 +158,10 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     uint32_t* const claim = sched + kMaxGrid * kMaxGrid;
     uint32_t* const cursor = sched + 2 * kMaxGrid * kMaxGrid;
     uint32_t* const events = cursor + kMaxGrid;
+    uint32_t* const claim2 = events + 1 + kMaxGrid; // after the arrival counters
     uint32_t* const stamps = trace ? reinterpret_cast<uint32_t*>(trace) + (int64_t)s * s : nullptr;
+    // after the event stamps: the same two moments on the 100 MHz realtime clock (low 32 bits)
+    uint32_t* const clocks = trace ? stamps + 2 * (int64_t)s * s : nullptr;
     // two private rows per wavefront of the grid for skipped stores
     T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
 
@@ -163,12 +179,14 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     for (;;) {
         int cw = s;
         bool open = false;
+        uint32_t prio = 0;
         if (lt >= 0) {
             cw = (int)__hip_atomic_load(cursor + lt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (cw < s) {
                 const int col = Cperm[(lt + Ooff[cw]) % s];
                 open = free_run ||
                        __hip_atomic_load(tickets + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= (uint32_t)cw;
+                prio = colw ? colw[col] : 0u;
             }
         }
         if (__builtin_amdgcn_ballot_w64(cw < s) == 0)
@@ -187,32 +205,69 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             continue;
         }
         polls = 0;
-        const int j = (int)__builtin_ctzll(avail);
+        // the first open block in preference order (home team first), unless
+        // an open block lies in a heavier critical column
+        int j = (int)__builtin_ctzll(avail);
+        if (colw) {
+            uint32_t best = __builtin_amdgcn_readlane(prio, j);
+            for (uint64_t rest = avail & (avail - 1); rest; rest &= rest - 1) {
+                const int l = (int)__builtin_ctzll(rest);
+                const uint32_t p = __builtin_amdgcn_readlane(prio, l);
+                if (p > best) {
+                    best = p;
+                    j = l;
+                }
+            }
+        }
         const int t = __builtin_amdgcn_readlane(lt, j);
         const int w = __builtin_amdgcn_readlane(cw, j);
         const int col = Cperm[(t + Ooff[w]) % s];
         const int64_t tw = (int64_t)t * s + w;
         const int64_t b = (int64_t)t * s + col;
         const int64_t lo = bstart[b], hi = bstart[b + 1];
-        const uint32_t nb = (uint32_t)((hi - lo + f - 1) / f);
-        uint32_t idx = 0;
-        if (lane == 0)
-            idx = __hip_atomic_fetch_add(claim + tw, kClaim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // Claims are counted in units of kUnit samples: head claims of f
+        // samples (two batches with HALF) from counter A while the block has
+        // more than `tail` units left unclaimed, then single units from
+        // counter B, so the block's last work is spread over many wavefronts
+        // in small pieces instead of a few whole batches.
+        const uint32_t nu = (uint32_t)((hi - lo + kUnit - 1) / kUnit);
+        const uint32_t big = kClaim * (uint32_t)f / kUnit;
+        const uint32_t split = tail > 0 ? (nu > tail ? (nu - tail) / big * big : 0u) : nu;
+        const uint32_t heads = (split + big - 1) / big;
+        uint32_t idx = 0, take = 0, got = 0;
+        if (lane == 0) {
+            const uint32_t a = __hip_atomic_fetch_add(claim + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a < heads) {
+                idx = a * big;
+                take = split - idx < big ? split - idx : big;
+            } else {
+                const uint32_t k = __hip_atomic_fetch_add(claim2 + tw, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                idx = split + k;
+                take = idx < nu ? 1u : 0u;
+                got = k; // 0 for the first claimant of an exhausted block
+            }
+        }
         idx = __builtin_amdgcn_readfirstlane(idx);
-        if (idx >= nb) {
+        take = __builtin_amdgcn_readfirstlane(take);
+        got = __builtin_amdgcn_readfirstlane(got);
+        if (take == 0) {
             // nothing left to claim in this block: move the team's cursor on;
             // an empty block is released by its only claimant
             if (lane == 0) {
-                if (nb == 0 && idx == 0) {
+                if (nu == 0 && got == 0) {
                     if (trace) {
                         trace[tw] = col;
                         const uint32_t e =
                             __hip_atomic_fetch_add(events, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         stamps[2 * tw] = e;
                         stamps[2 * tw + 1] = e + 1u;
+                        const uint32_t now = (uint32_t)__builtin_amdgcn_s_memrealtime();
+                        clocks[2 * tw] = now;
+                        clocks[2 * tw + 1] = now;
                         __builtin_amdgcn_s_waitcnt(0);
                     }
-                    __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+                    release_agent();
+                    __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
                 uint32_t expect = (uint32_t)w;
                 __hip_atomic_compare_exchange_strong(cursor + t, &expect, (uint32_t)(w + 1), __ATOMIC_RELAXED,
@@ -225,6 +280,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
                 trace[tw] = col;
             const uint32_t e = __hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_fetch_min(stamps + 2 * tw, e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (idx == 0)
+                clocks[2 * tw] = (uint32_t)__builtin_amdgcn_s_memrealtime();
             __builtin_amdgcn_s_waitcnt(0); // stamped before any of the batch's rows is read
         }
         if (entered != tw) {
@@ -233,10 +290,10 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             entered = tw;
         }
-        const int64_t b0 = lo + (int64_t)idx * f;
-        const int64_t span = (int64_t)kClaim * f;
+        const int64_t b0 = lo + (int64_t)idx * kUnit;
+        const int64_t span = (int64_t)take * kUnit;
         const int64_t cnt = hi - b0 < span ? hi - b0 : span;
-        const uint32_t ran = cnt > f ? 2u : 1u; // batches this claim covers
+        const uint32_t ran = take; // units this claim covers
         DebugSink blk = dbg;
         blk.trace = nullptr;
         if (blk.orig)
@@ -253,14 +310,16 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
         if (lane == 0)
             done = __hip_atomic_fetch_add(fin + tw, ran, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         done = __builtin_amdgcn_readfirstlane(done);
-        if (done + ran == nb) {
+        if (done + ran == nu) {
             // last batch of the block: every batch's stores are in this XCD's
-            // L2; write it back, then pass the column on
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            // L2; write it back, wait for the write-back, then pass the
+            // column on
+            release_agent();
             if (lane == 0) {
                 if (trace) {
                     stamps[2 * tw + 1] =
                         __hip_atomic_fetch_add(events, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    clocks[2 * tw + 1] = (uint32_t)__builtin_amdgcn_s_memrealtime();
                     __builtin_amdgcn_s_waitcnt(0);
                 }
                 __hip_atomic_store(tickets + col, (uint32_t)(w + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -413,7 +472,7 @@ __global__ __launch_bounds__(64) void k_table(const Sample* __restrict__ Sp, con
         run_worker<KP, T, D, DBG, false>(Sp + lo, hi - lo, 1, 0, f, P, Q, lr, lp, lq, blk);
         // the block's stores reach memory before its row and column are free
         __builtin_amdgcn_s_waitcnt(0);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        release_agent();
         if (lane == 0) {
             if (DBG && trace) {
                 trace[3 * (int64_t)d + 2] =
@@ -633,8 +692,8 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (KP == 32) {
             if (a.half && !a.sink) {
                 hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool,
-                                   a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw,
+                                   a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
             }
@@ -642,8 +701,8 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (D == 1 && (sizeof(T) == 4 || Geo<KP>::E % 2 == 0)) {
             if (a.atomic) {
                 hipLaunchKernelGGL((k_blocked<KP, T, 1, DBG, false, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool,
-                                   a.free_run, a.sigma_c, a.sigma_o, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw,
+                                   a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
             }
@@ -653,12 +712,12 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)a.sink, acoh);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.free_run, a.sigma_c, a.sigma_o, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)nullptr, acoh);
     }
@@ -791,11 +850,13 @@ struct Dispatch {
     static int occupancy(int KP, int depth, bool half)
     {
         switch (KP) {
+        // half: the two-workers-per-wavefront kernel wherever it runs (its
+        // lanes hold twice the values, so fewer of its wavefronts fit a CU)
         case 32: return occupancy_kp<32, T>(depth, half);
-        case 64: return occupancy_kp<64, T>(depth, false);
-        case 128: return occupancy_kp<128, T>(depth, false);
-        case 256: return occupancy_kp<256, T>(depth, false);
-        case 512: return occupancy_kp<512, T>(depth, false);
+        case 64: return occupancy_kp<64, T>(depth, half);
+        case 128: return occupancy_kp<128, T>(depth, half);
+        case 256: return occupancy_kp<256, T>(depth, half);
+        case 512: return occupancy_kp<512, T>(depth, half);
         default: return 0;
         }
     }

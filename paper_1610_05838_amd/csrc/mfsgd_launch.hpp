@@ -14,9 +14,9 @@ constexpr int kRmseWaves = 2048;  // fixed, so the RMSE reduction order never ch
 constexpr int kSchemeHogwild = 0;
 constexpr int kSchemeWavefront = 1;
 constexpr int kSchemeWaveLaunch = 2; // one deterministic wavefront-update wave per launch (cross-check)
-// block-scheduled claim state: finished and claimed batches per (team, wave), cursor per team, event counter,
-// workgroups arrived per XCD
-constexpr int kSchedWords = 2 * kMaxGrid * kMaxGrid + kMaxGrid + 1 + kMaxGrid;
+// block-scheduled claim state: finished units and head claims per (team, wave), cursor per team, event counter,
+// workgroups arrived per XCD, unit claims (after the head claims) per (team, wave)
+constexpr int kSchedWords = 3 * kMaxGrid * kMaxGrid + kMaxGrid + 1 + kMaxGrid;
 
 struct DebugSink;
 
@@ -50,10 +50,12 @@ struct EpochLaunch {
                            // one-wavefront teams: per workgroup
     const int32_t* xteams; // per XCD x: [x * (kMaxGrid + 1)] = team count, then the teams placed on x
     int pool;              // 1: a wavefront also serves the other teams of its XCD
+    const uint32_t* colw;  // pooled: per column block a priority weight (0: none), or nullptr
     int free_run;          // 1: blocks open without waiting for their column ticket
     int wg_waves;    // wavefronts per workgroup
     void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
     uint64_t sigma_c, sigma_o;
+    uint32_t tail;   // pooled teams: units (64 samples) of a block claimed one at a time at its end (0: none)
     int wave;        // kSchemeWaveLaunch: the wave this launch runs
     uint32_t* tickets;
     uint32_t* sched; // claim state, kSchedWords entries (see k_blocked)

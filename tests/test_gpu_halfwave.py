@@ -226,7 +226,8 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
     scheme = "hogwild"
     rng = np.random.default_rng(s * 31 + skip)
     f = 64
-    S, m, n = disjoint_block_samples(rng, s, f, 6, 3, 2)
+    G, gu, gv = 6, 3, 2
+    S, m, n = disjoint_block_samples(rng, s, f, G, gu, gv)
     k, seed = 32, 123 + s
     opts = dict(batch_f=f, balance=0, partition=1, hogwild_grid=s, skip_stores=skip)
     res = {}
@@ -246,11 +247,56 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
         P, Q = M.get_factors(m, n, k)
         res[half] = (P.cpu().numpy().astype(dtype), Q.cpu().numpy().astype(dtype))
     (Ph, Qh), (Pf, Qf) = res[1], res[0]
-    assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf))
     Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
     for t in range(2):
         oracle.epoch_wavefront(Po, Qo, S, 0.01, 0.05, 0.04, s, seed, t, balanced=False)
-    assert maxabs(Ph, Po) <= TOL[dtype] and maxabs(Qh, Qo) <= TOL[dtype]
+    for half, (P, Q) in res.items():
+        # name the rows (and their blocks) that left the schedule's result
+        dP = np.abs(P.astype(np.float64) - Po).max(axis=1)
+        dQ = np.abs(Q.astype(np.float64) - Qo).max(axis=1)
+        badP, badQ = np.nonzero(dP > TOL[dtype])[0], np.nonzero(dQ > TOL[dtype])[0]
+        where = (f"half_waves={half}: P rows {badP[:8].tolist()} (blocks {(badP[:8] // (G * gu)).tolist()}), "
+                 f"Q rows {badQ[:8].tolist()} (column blocks {(badQ[:8] // (G * gv)).tolist()}), "
+                 f"max {dP.max():.3g} / {dQ.max():.3g}")
+        print(where)
+        assert badP.size == 0 and badQ.size == 0, where
+    assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf))
+
+
+@pytest.mark.parametrize("half", [1, 0])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("s", [8, 16])
+def test_block_scheduled_runs_repeat_bit_for_bit(M, dtype, s, half):
+    """Column hand-over under load: blocks of at most a few batches, so the
+    next block in a column is claimed the moment its ticket moves and its
+    first batch reads the rows the previous block wrote on another XCD.  On
+    data whose concurrently runnable batches commute, every run of the
+    schedule is the same computation, so repeated runs agree bit for bit
+    (a ticket seen before the releasing XCD's L2 write-back has finished
+    shows up as a lost update in some column's first batch)."""
+    rng = np.random.default_rng(1000 + s)
+    f = 64
+    S, m, n = disjoint_block_samples(rng, s, f, 3, 3, 2)
+    k, seed = 32, 7 + s
+    first = None
+    for rep in range(6):
+        o = dict(DEFAULTS, dtype=1 if dtype == np.float16 else 0, half_waves=half, batch_f=f, balance=0,
+                 partition=1, hogwild_grid=s, skip_stores=0)
+        M.reset_options()
+        for key, val in o.items():
+            M.set_option(key, val)
+        M.init(m, n, k, seed)
+        dS = M.samples_to_device(S)
+        for _ in range(3):
+            M.epoch(dS, 0.01, 0.05, 0.04, "hogwild")
+        P, Q = (x.cpu().numpy().astype(dtype) for x in M.get_factors(m, n, k))
+        if first is None:
+            first = (P, Q)
+            continue
+        rows_p = np.nonzero(np.any(bits(P) != bits(first[0]), axis=1))[0]
+        rows_q = np.nonzero(np.any(bits(Q) != bits(first[1]), axis=1))[0]
+        assert rows_p.size == 0 and rows_q.size == 0, \
+            f"run {rep}: P rows {rows_p[:8].tolist()}, Q rows {rows_q[:8].tolist()} differ from run 0"
 
 
 @pytest.mark.parametrize("scheme,s,opts", [
