@@ -282,7 +282,6 @@ def measure(args, name, scheme, steps, warmup, dev, host_prefix=0):
     dtype = 1 if w["dtype"] == "fp16" else 0
     apply_options(mfsgd, args, dtype)
     mfsgd.init(w["m"], w["n"], w["k"], w["seed"])
-    kernel = kernel_of(mfsgd, scheme, args.staged)
     grid_s = args.grid_s or w.get("grid_s", 32)
     if scheme == "table":
         grid_s = mfsgd.get_option("table_grid")
@@ -310,6 +309,8 @@ def measure(args, name, scheme, steps, warmup, dev, host_prefix=0):
     for t in range(warmup):
         rmses.append(step(t))
         log(f"{name} warmup epoch {t}: test rmse {rmses[-1]:.5f}")
+    # the automatic batch-Hogwild! form is chosen per sample array at the first epoch
+    kernel = kernel_of(mfsgd, scheme, args.staged)
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -320,9 +321,13 @@ def measure(args, name, scheme, steps, warmup, dev, host_prefix=0):
     epoch_ms = [a.elapsed_time(b) for a, b in events]
     log(f"{name}: timed {steps} steps in {wall:.3f}s; epoch kernel ms: " + ", ".join(f"{x:.2f}" for x in epoch_ms))
     log(f"{name}: test rmse after each epoch: " + ", ".join(f"{x:.4f}" for x in rmses))
+    form = mfsgd.get_option("hogwild_form") if scheme == "hogwild" and not args.staged else -1
+    atomic = mfsgd.get_option("hogwild_atomic") if form >= 0 else 0
     r = dict(w=w, scheme=scheme, grid_s=grid_s, nnz=nnz, ntest=len(T), epoch_ms=epoch_ms, rmses=rmses, wall=wall,
              kernel=kernel, S=S, dtype=dtype, resident=mfsgd.get_option("resident_waves"),
-             partitioned=scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged)
+             partitioned=scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged,
+             form={-1: "", 0: "one address space", 1: "XCD-partitioned", 3: "XCD-partitioned, free-running",
+                   4: "one XCD"}.get(form, str(form)) + (", atomic adds" if atomic else ""))
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -451,7 +456,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if r["dtype"] == 0 else "f16-storage/f32-math",
         "data": f"synthetic (seeded planted low-rank model with the {w['name']} shape)",
-        "config": {"workload": describe(r), "scheme": scheme, "partitioned": r["partitioned"],
+        "config": {"workload": describe(r), "scheme": scheme, "form": r["form"] or None,
                    "workers": args.workers or "auto", "staged": args.staged, "resident_waves": r["resident"],
                    "depth": args.depth or "auto", "epochs_timed": args.steps},
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -487,7 +492,7 @@ def main():
             e = measure(args, name, "hogwild", args.extra_steps, 1, dev)
             bpu, avg_s, gbs = rates(e)
             extra.append({"workload": describe(e), "scheme": "hogwild",
-                          "form": "one XCD" if e["partitioned"] else "one address space", "kernel": e["kernel"],
+                          "form": e["form"], "kernel": e["kernel"],
                           "epochs_timed": args.extra_steps, "median_epoch_ms": sorted(e["epoch_ms"])[len(e["epoch_ms"]) // 2],
                           "epoch_updates_per_s": e["nnz"] / avg_s, "bytes_per_update": bpu,
                           "algorithmic_gbs": gbs, "frac": gbs / HBM_PEAK_GBS,
