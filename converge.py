@@ -106,20 +106,21 @@ class Runner:
         self.w = w
         log(f"generated {workload}: {w['ntrain']} train + {w['ntest']} test in {time.perf_counter() - t0:.1f}s")
 
-    def setup(self, scheme, s, workers=0, partition=0):
+    def setup(self, scheme, s, workers=0, partition=2):
         """Initialise (and plan); returns the number of concurrent workers
         (wavefronts) the launch will have, 0 for the library's default.
         A wavefront-update grid of side s runs s teams of team_waves
         wavefronts, grouped four to a workgroup (one-wavefront teams when
         workers == s)."""
         w, M = self.w, self.M
+        # every option at the library's default except those named here
+        M.reset_options()
+        M.set_option("dtype", 1 if w["dtype"] == "fp16" else 0)
         if scheme == "table":
             W = workers or 128
             grid = s or min(1024, 2 * W)
-            opts = dict(dtype=1 if w["dtype"] == "fp16" else 0, batch_f=256, depth=2, table_grid=grid,
-                        table_workers=W, debug=0)
-            for key, val in opts.items():
-                M.set_option(key, val)
+            M.set_option("table_grid", grid)
+            M.set_option("table_workers", W)
             M.init(w["m"], w["n"], w["k"], w["seed"])
             return W
         s = s or w.get("grid_s", 32)
@@ -128,10 +129,11 @@ class Runner:
         if scheme != "hogwild" and workers > 0:
             team = max(1, workers // s)
             actual = s if team == 1 else s * 4 * ((team + 3) // 4)
-        opts = dict(dtype=1 if w["dtype"] == "fp16" else 0, batch_f=256, workers=workers if scheme == "hogwild" else 0,
-                    depth=2, team_waves=team, partition=partition, debug=0)
-        for key, val in opts.items():
-            M.set_option(key, val)
+        if scheme == "hogwild":
+            M.set_option("workers", workers)
+            M.set_option("partition", partition)
+        else:
+            M.set_option("team_waves", team)
         M.init(w["m"], w["n"], w["k"], w["seed"])
         if scheme != "hogwild":
             M.plan(self.dS, s)
@@ -228,8 +230,9 @@ def main():
     ap.add_argument("--lr", choices=["config", "paper"], default="config")
     ap.add_argument("--schemes", default="")
     ap.add_argument("--target", type=float, default=0.92)
-    ap.add_argument("--partition", type=int, default=0,
-                    help="batch-Hogwild! form: 0 one address space, 1 XCD-partitioned, 2 automatic")
+    ap.add_argument("--partition", type=int, default=2,
+                    help="batch-Hogwild! form (the library's option): 2 automatic (default), 0 one address "
+                         "space, 1 XCD-partitioned, 3 free-running partition, 4 one XCD")
     ap.add_argument("--counts", default="32,64,128,256,512,1024,2048,4096,8192")
     ap.add_argument("--uniform", action="store_true", help="users and items drawn uniformly (no Zipf skew)")
     args = ap.parse_args()

@@ -171,11 +171,12 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  blocks allow).  A worker's wavefronts prefer its blocks
  *                  but also serve the other workers on their XCD.
  *   "priority"     pooled block-scheduled epochs: 1 (default) a wavefront
- *                  that finds several open blocks takes the one whose
- *                  column block holds the most samples among the columns
- *                  holding over 1.5 times the mean (such a column's chain of
- *                  blocks bounds the epoch); otherwise, and with 0, its own
- *                  worker's block first.
+ *                  that finds several open blocks takes the one with the
+ *                  most work chained behind it (MFSGD_DBG_PRIORITY: the
+ *                  epoch's critical path runs through it, e.g. the blocks
+ *                  of a column holding far more than its share, and the
+ *                  blocks that gate them); among equals, and with 0, its
+ *                  own worker's block first.
  *   "tail_claims"  pooled block-scheduled epochs: 1 claims a block's last
  *                  2 units of 64 samples per wavefront of the XCD one unit
  *                  at a time instead of in batches of f; 0 (default).
@@ -430,6 +431,14 @@ int64_t mfsgd_get_epoch(void);
  *   MFSGD_DBG_TABLE_ORDER  : same plan, count <= nnz, dst int64 -- position in
  *                      the caller's array of each planned sample (needs a plan
  *                      made while debug bit 0 was set).
+ *   MFSGD_DBG_PRIORITY : the critical-path weights of the last pooled
+ *                      block-scheduled epoch with "priority" on: count = s*s,
+ *                      dst uint32 -- entry t*s + w for team t's block of wave
+ *                      w: the largest number of 64-sample units (each block
+ *                      rounded up) on a chain from that block to the end of
+ *                      the epoch, where a block is followed by the same
+ *                      team's block of the next wave and by the next wave's
+ *                      block in its column.
  * dst may be host or device memory. */
 enum {
     MFSGD_DBG_VISITS = 1,
@@ -439,7 +448,8 @@ enum {
     MFSGD_DBG_TEAM_MAP = 5,
     MFSGD_DBG_TEAM_SIZES = 6,
     MFSGD_DBG_TABLE_STARTS = 7,
-    MFSGD_DBG_TABLE_ORDER = 8
+    MFSGD_DBG_TABLE_ORDER = 8,
+    MFSGD_DBG_PRIORITY = 9
 };
 int mfsgd_debug_read(int32_t what, void* dst, int64_t count, void* stream);
 

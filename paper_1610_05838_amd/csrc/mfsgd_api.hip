@@ -84,7 +84,6 @@ struct Plan {
     int64_t orig_cap = 0;
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
-    uint32_t* colw = nullptr;    // kMaxGrid: priority weight of each column block (0: none)
     double hot_col = 0.0;        // largest share of a column block's samples held by one item
     double hot_row = 0.0;        // largest share of a row block's samples held by one user
     uint64_t version = 0;        // bumped by every build
@@ -140,6 +139,8 @@ struct Context {
     void* P = nullptr;
     void* Q = nullptr;
     uint32_t* tickets = nullptr;
+    uint32_t* prio = nullptr; // kMaxGrid^2: critical-path weight per (team, wave) of the last pooled epoch
+    int prio_s = 0;           // its grid side (0: none yet)
     uint32_t* sched = nullptr; // block-scheduled claim state (kSchedWords)
     int* err = nullptr;
     int* bad = nullptr;
@@ -261,7 +262,6 @@ int grow(T** p, int64_t* cap, int64_t need, const char* what)
 
 void free_plan(Plan& p)
 {
-    dfree(p.colw);
     dfree(p.Sp);
     dfree(p.orig);
     dfree(p.bstart);
@@ -284,6 +284,7 @@ void release_all()
     dfree(c.P);
     dfree(c.Q);
     dfree(c.tickets);
+    dfree(c.prio);
     dfree(c.sched);
     dfree(c.err);
     dfree(c.bad);
@@ -612,6 +613,7 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     int rc;
     if ((rc = dalloc(&c.P, (size_t)m * c.KP * es, "P")) || (rc = dalloc(&c.Q, (size_t)n * c.KP * es, "Q")) ||
         (rc = dalloc((void**)&c.tickets, sizeof(uint32_t) * kMaxGrid, "tickets")) ||
+        (rc = dalloc((void**)&c.prio, sizeof(uint32_t) * kMaxGrid * kMaxGrid, "block priorities")) ||
         (rc = dalloc((void**)&c.sched, sizeof(uint32_t) * kSchedWords, "claim counters")) ||
         (rc = dalloc((void**)&c.err, sizeof(int), "flag")) || (rc = dalloc((void**)&c.bad, sizeof(int), "flag")) ||
         (rc = dalloc((void**)&c.partial, sizeof(double) * kRmseWaves, "rmse partials")) ||
@@ -772,8 +774,6 @@ int build_hot(const mfsgd_sample* samples, int64_t nnz, int log2, hipStream_t st
     return MFSGD_OK;
 }
 
-constexpr double kCriticalRatio = 1.5;
-
 int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool balanced, bool keep_orig,
                hipStream_t st)
 {
@@ -854,25 +854,6 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     HIPCHK(hipMemcpyAsync(pl.hstart.data(), pl.bstart, sizeof(int64_t) * pl.hstart.size(), hipMemcpyDeviceToHost,
                           st));
     HIPCHK(hipStreamSynchronize(st));
-    // Column priorities for pooled wavefronts: a column block holding well
-    // over its share of the samples is worked by one team after another for
-    // the whole epoch (its chain of blocks bounds the epoch), so a wavefront
-    // that finds several open blocks takes the one in the heaviest such
-    // column.  Columns within kCriticalRatio of the mean get no priority.
-    {
-        std::vector<uint32_t> w(kMaxGrid, 0u);
-        std::vector<int64_t> col(s, 0);
-        for (int t = 0; t < s; ++t)
-            for (int j = 0; j < s; ++j)
-                col[j] += pl.hstart[(size_t)t * s + j + 1] - pl.hstart[(size_t)t * s + j];
-        const double mean = (double)nnz / (double)s;
-        for (int j = 0; j < s; ++j)
-            if ((double)col[j] > kCriticalRatio * mean)
-                w[j] = (uint32_t)std::min<int64_t>(col[j] / 64 + 1, 0xffffffffll);
-        if (!pl.colw)
-            CHK(dalloc((void**)&pl.colw, sizeof(uint32_t) * kMaxGrid, "column priorities"));
-        HIPCHK(hipMemcpy(pl.colw, w.data(), sizeof(uint32_t) * kMaxGrid, hipMemcpyHostToDevice));
-    }
     pl.version += 1;
     pl.src = samples;
     pl.nnz = nnz;
@@ -1217,7 +1198,6 @@ int team_layout(const Plan& pl, int64_t want, bool half, EpochLaunch& a)
     a.pool = want == 1 ? 0 : 1;
     a.wg_waves = waves;
     a.sink = skip_stores(pl) ? c.sink : nullptr;
-    a.colw = g_opt.priority && a.pool ? pl.colw : nullptr;
     // the last 2 units per wavefront of the XCD go one unit per claim
     a.tail = a.pool && g_opt.tail_claims ? (uint32_t)std::min<int64_t>(2 * (int64_t)c.lay_xslots * waves, 1 << 30) : 0u;
     a.half = 0;
@@ -1400,6 +1380,12 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         }
         a.sigma_c = sm64_at(c.seed, kTagColPerm + 2ull * (uint64_t)c.epoch);
         a.sigma_o = sm64_at(c.seed, kTagWaveOffset + 2ull * (uint64_t)c.epoch);
+        a.prio = nullptr;
+        if (a.pool && g_opt.priority) {
+            HIPCHK(block_priority(a.bstart, s, a.sigma_c, a.sigma_o, c.prio, st));
+            a.prio = c.prio;
+            c.prio_s = s;
+        }
         a.tickets = c.tickets;
         a.sched = c.sched;
         a.free_run = hog && form == 3 ? 1 : 0;
@@ -1694,6 +1680,12 @@ int debug_read_impl(int32_t what, void* dst, int64_t count, hipStream_t st)
         if (count)
             HIPCHK(hipMemcpyAsync(dst, what == MFSGD_DBG_TEAM_MAP ? c.tmap : c.tsize, sizeof(int32_t) * (size_t)count,
                                   hipMemcpyDefault, st));
+    } else if (what == MFSGD_DBG_PRIORITY) {
+        if (c.prio_s == 0)
+            return fail(MFSGD_ESTATE, "no block-scheduled epoch with priorities has run");
+        if (count != (int64_t)c.prio_s * c.prio_s)
+            return fail(MFSGD_EINVAL, "count must be s*s of the last epoch with priorities");
+        HIPCHK(hipMemcpyAsync(dst, c.prio, sizeof(uint32_t) * (size_t)count, hipMemcpyDefault, st));
     } else {
         return fail(MFSGD_EINVAL, "unknown debug buffer");
     }

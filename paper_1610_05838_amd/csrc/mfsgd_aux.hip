@@ -70,6 +70,53 @@ hipError_t reset_tickets(uint32_t* tickets, uint32_t* sched, hipStream_t st)
     return hipGetLastError();
 }
 
+// Critical-path priorities of a block-scheduled epoch.  Block (t, w) is team
+// t's block of wave w, column C[(t + O[w]) mod s]; it must be exhausted
+// before the same team's block of wave w+1 can be claimed, and completed
+// before the column's block of wave w+1 (team (t + O[w] - O[w+1]) mod s)
+// opens.  prio[t*s + w] = the largest number of 64-sample units on a chain
+// of such successors from (t, w) to the end of the epoch, its own included:
+// the work that still has to follow this block one step at a time.  One
+// workgroup, lane t for team t, waves from the last to the first.
+__global__ __launch_bounds__(kMaxGrid) void k_block_priority(const int64_t* __restrict__ bstart, int s,
+                                                            uint64_t sigma_c, uint64_t sigma_o,
+                                                            uint32_t* __restrict__ prio)
+{
+    __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
+    __shared__ uint64_t chain[kMaxGrid];
+    const int t = threadIdx.x;
+    if (t == 0) {
+        shuffle_perm(sigma_c, s, Cperm);
+        shuffle_perm(sigma_o, s, Ooff);
+    }
+    chain[t] = 0;
+    __syncthreads();
+    for (int w = s - 1; w >= 0; --w) {
+        uint64_t v = 0;
+        if (t < s) {
+            const int64_t b = (int64_t)t * s + Cperm[(t + Ooff[w]) % s];
+            v = (uint64_t)((bstart[b + 1] - bstart[b] + 63) / 64);
+            if (w + 1 < s) {
+                const int tc = ((t + Ooff[w] - Ooff[w + 1]) % s + s) % s;
+                v += chain[t] > chain[tc] ? chain[t] : chain[tc];
+            }
+        }
+        __syncthreads();
+        if (t < s) {
+            chain[t] = v;
+            prio[(int64_t)t * s + w] = v > 0xffffffffull ? 0xffffffffu : (uint32_t)v;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t block_priority(const int64_t* bstart, int s, uint64_t sigma_c, uint64_t sigma_o, uint32_t* prio,
+                          hipStream_t st)
+{
+    hipLaunchKernelGGL(k_block_priority, dim3(1), dim3(kMaxGrid), 0, st, bstart, s, sigma_c, sigma_o, prio);
+    return hipGetLastError();
+}
+
 // Which XCD (accelerator complex die) runs each workgroup: the hardware
 // register XCC_ID of gfx94x/gfx950.
 __global__ void k_probe_xcc(int* out)

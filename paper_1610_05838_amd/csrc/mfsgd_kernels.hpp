@@ -89,10 +89,11 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // Claims are counted in units of 64 samples: a block's first units go in
 // head claims of f samples (2 f with HALF), its last `tail` units one at a
 // time, so that the block ends with many wavefronts finishing small pieces.
-// Among the open blocks a wavefront can serve, it takes the first in its
-// preference order (home team first) unless colw gives another one's
-// column a higher weight (a column holding well over its share of the
-// samples is a chain of blocks that bounds the epoch).
+// Among the open blocks a wavefront can serve, it takes the one with the
+// largest critical-path weight prio[t*s + w] (the work that must still
+// follow the block one step at a time: the team's later blocks and the
+// column's, k_block_priority), the first in its preference order (home team
+// first) among equals or when prio is null.
 //
 // sched: [0, G2) units finished per (team, wave), [G2, 2 G2) head claims
 // taken per (team, wave), [2 G2, 2 G2 + kMaxGrid) cursor per team, one event
@@ -114,7 +115,7 @@ template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false, boo
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,
                                                  int s, int xslots, const int32_t* __restrict__ tmap,
                                                  const int32_t* __restrict__ xteams, int nx, int pool,
-                                                 const uint32_t* __restrict__ colw, int free_run,
+                                                 const uint32_t* __restrict__ prio_tw, int free_run,
                                                  uint64_t sigma_c, uint64_t sigma_o, uint32_t tail, T* __restrict__ P,
                                                  T* __restrict__ Q, float lr, float lp, float lq, int f,
                                                  uint32_t* tickets, uint32_t* sched, uint32_t spin_limit, int* err,
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
                 const int col = Cperm[(lt + Ooff[cw]) % s];
                 open = free_run ||
                        __hip_atomic_load(tickets + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= (uint32_t)cw;
-                prio = colw ? colw[col] : 0u;
+                prio = prio_tw ? prio_tw[(int64_t)lt * s + cw] : 0u;
             }
         }
         if (__builtin_amdgcn_ballot_w64(cw < s) == 0)
@@ -205,10 +206,10 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
             continue;
         }
         polls = 0;
-        // the first open block in preference order (home team first), unless
-        // an open block lies in a heavier critical column
+        // the open block with the longest chain behind it, the first in
+        // preference order (home team first) among equals
         int j = (int)__builtin_ctzll(avail);
-        if (colw) {
+        if (prio_tw) {
             uint32_t best = __builtin_amdgcn_readlane(prio, j);
             for (uint64_t rest = avail & (avail - 1); rest; rest &= rest - 1) {
                 const int l = (int)__builtin_ctzll(rest);
@@ -692,7 +693,7 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (KP == 32) {
             if (a.half && !a.sink) {
                 hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.prio,
                                    a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
@@ -701,7 +702,7 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         if constexpr (D == 1 && (sizeof(T) == 4 || Geo<KP>::E % 2 == 0)) {
             if (a.atomic) {
                 hipLaunchKernelGGL((k_blocked<KP, T, 1, DBG, false, false, true>), dim3((unsigned)a.grid),
-                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw,
+                                   dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.prio,
                                    a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
@@ -712,12 +713,12 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
         // skipped stores only in epochs without debug output (they never change results)
         if (!DBG && a.sink)
             hipLaunchKernelGGL((k_blocked<KP, T, D, false, true>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.prio, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)a.sink, acoh);
         else
             hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false>), dim3((unsigned)a.grid), dim3(64 * a.wg_waves), 0,
-                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.colw, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
+                               st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.prio, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q,
                                a.lr, a.lp, a.lq, a.f, a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave,
                                (T*)nullptr, acoh);
     }

@@ -50,7 +50,7 @@ struct EpochLaunch {
                            // one-wavefront teams: per workgroup
     const int32_t* xteams; // per XCD x: [x * (kMaxGrid + 1)] = team count, then the teams placed on x
     int pool;              // 1: a wavefront also serves the other teams of its XCD
-    const uint32_t* colw;  // pooled: per column block a priority weight (0: none), or nullptr
+    const uint32_t* prio;  // pooled: per (team, wave) t*s+w a critical-path weight, or nullptr
     int free_run;          // 1: blocks open without waiting for their column ticket
     int wg_waves;    // wavefronts per workgroup
     void* sink;      // grid * wg_waves * 2 * KP storage elements: rows for skipped stores (nullptr: no skipping)
@@ -121,6 +121,8 @@ hipError_t rmse_final(const double* partial, int64_t ntest, double* out, hipStre
 hipError_t check_indices(const Sample* S, int64_t nnz, int64_t m, int64_t n, int* bad, hipStream_t st);
 // zero the column tickets and the kSchedWords claim counters (a fill kernel, safe under graph capture)
 hipError_t reset_tickets(uint32_t* tickets, uint32_t* sched, hipStream_t st);
+hipError_t block_priority(const int64_t* bstart, int s, uint64_t sigma_c, uint64_t sigma_o, uint32_t* prio,
+                          hipStream_t st);
 // XCC id of each of `n` one-wavefront workgroups (to learn the dispatch layout)
 hipError_t probe_xcc(int* out, int n, hipStream_t st);
 // stable bucketing of samples into the s x s grid

@@ -26,7 +26,7 @@ OK, EINVAL, ENOMEM, EHIP, ESTATE, ETIMEOUT, ENUMERIC = 0, -1, -2, -3, -4, -5, -6
 BATCH_HOGWILD, WAVEFRONT, WAVEFRONT_DET, GLOBAL_TABLE = 0, 1, 2, 3
 FP32, FP16 = 0, 1
 DBG_VISITS, DBG_TRACE, DBG_PLAN_STARTS, DBG_PLAN_ORDER, DBG_TEAM_MAP, DBG_TEAM_SIZES = 1, 2, 3, 4, 5, 6
-DBG_TABLE_STARTS, DBG_TABLE_ORDER = 7, 8
+DBG_TABLE_STARTS, DBG_TABLE_ORDER, DBG_PRIORITY = 7, 8, 9
 
 SCHEMES = {"hogwild": BATCH_HOGWILD, "wavefront": WAVEFRONT, "wavefront_det": WAVEFRONT_DET,
            "table": GLOBAL_TABLE}
@@ -264,6 +264,15 @@ def debug_team_layout(s: int, stream=None):
     _check(lib().mfsgd_debug_read(DBG_TEAM_SIZES, C.c_void_p(sizes.data_ptr()), s, _stream(stream)),
            "mfsgd_debug_read")
     return tmap[:grid], sizes
+
+
+def debug_priority(s: int, stream=None):
+    """Critical-path weight of every (team, wave) block of the last pooled
+    block-scheduled epoch: uint32 tensor of s*s, entry t*s + w."""
+    out = torch.empty(s * s, dtype=torch.int32, device="cuda")
+    _check(lib().mfsgd_debug_read(DBG_PRIORITY, C.c_void_p(out.data_ptr()), s * s, _stream(stream)),
+           "mfsgd_debug_read")
+    return out
 
 
 def finalize() -> None:

@@ -244,6 +244,41 @@ def test_team_layout_follows_row_loads(M, s):
     assert len(set(xcd.values())) == min(s, nx)
 
 
+@pytest.mark.parametrize("s", [16, 7])
+def test_block_priorities_are_critical_paths(M, s):
+    """Pooled wavefront-update: the weight a wavefront ranks open blocks by
+    is, for team t's block of wave w, the largest number of 64-sample units
+    on a chain from that block to the end of the epoch, where a block is
+    followed by its team's block of the next wave and by the next wave's
+    block in its column (section 3.2.3's schedule: worker i takes column
+    sigma_i(w) in wave w; the column ticket orders a column's blocks).
+    Recomputed here from the plan's block starts and the oracle's sigma."""
+    rng = np.random.default_rng(17 + s)
+    m, n = 30_000, 5_000
+    S = rand_samples(rng, m, n, 300_000)
+    S["v"][:60_000] = 4321  # one item holds a fifth of the samples: its column dominates
+    setup(M, m, n, 64, 9, balance=0)
+    d = M.samples_to_device(S)
+    M.plan(d, s)
+    for t in range(2):
+        M.epoch(d, 0.01, 0.05, 0.05, "wavefront")
+        got = M.debug_priority(s).cpu().numpy().view(np.uint32).reshape(s, s)
+        starts = M.debug_plan_starts(s).cpu().numpy()
+        units = (np.diff(starts).reshape(s, s) + 63) // 64  # [row block, column block]
+        sig = oracle.wavefront_sigma(9, t, s)               # [team, wave] -> column block
+        team_in = np.empty((s, s), dtype=np.int64)          # [column, wave] -> team
+        for i in range(s):
+            team_in[sig[i], np.arange(s)] = i
+        want = np.zeros((s, s), dtype=np.int64)
+        for w in range(s - 1, -1, -1):
+            for i in range(s):
+                nxt = 0
+                if w + 1 < s:
+                    nxt = max(want[i, w + 1], want[team_in[sig[i, w], w + 1], w + 1])
+                want[i, w] = units[i, sig[i, w]] + nxt
+        assert np.array_equal(got.astype(np.int64), want)
+
+
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 def test_partitioned_hogwild_single_wave_teams_match_oracle(M, gen, dtype):
     """Partitioned batch-Hogwild! with one wavefront per team is the wavefront
