@@ -53,9 +53,9 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel_key: str, variant: list):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources with the same bench options
+def profile_record(kernel_key: str, variant: list):
+    """The committed rocprofv3 counter record of this kernel and workload, if
+    it was taken on the current kernel sources with the same bench options
     (`variant`: the options that change the launch); else None."""
     path = os.path.join(PROFILE_DIR, f"traffic_{kernel_key}.json")
     if not os.path.exists(path):
@@ -64,7 +64,13 @@ def measured_traffic(kernel_key: str, variant: list):
         d = json.load(f)
     if d.get("source_digest") != source_digest() or d.get("bench_args", []) != variant:
         return None
-    return d.get("hbm_bytes_per_launch")
+    return d
+
+
+def measured_traffic(kernel_key: str, variant: list):
+    """L2-to-fabric bytes per launch from the committed counter record, or None."""
+    d = profile_record(kernel_key, variant)
+    return d.get("hbm_bytes_per_launch") if d else None
 
 
 def _oracle_factors(w, S, dtype):
@@ -475,6 +481,19 @@ def main():
     if traffic:
         out["roofline"]["traffic_gbs"] = traffic / avg_epoch_s / 1e9
         out["roofline"]["traffic_frac"] = traffic / avg_epoch_s / 1e9 / HBM_PEAK_GBS
+    rec = profile_record(key, variant)
+    sq = (rec or {}).get("sq_per_launch") or {}
+    if sq.get("SQ_INSTS_VALU"):
+        # the bound that applies where the rows come from the caches: wave64
+        # vector instructions issued per second against what the chip can issue
+        peak = rec["valu_issue_peak_per_s"]
+        rate = sq["SQ_INSTS_VALU"] / avg_epoch_s
+        out["roofline_issue"] = {"bound": "valu-issue", "achieved": rate / 1e9, "peak": peak / 1e9,
+                                 "unit": "G wave64 vector instructions/s", "frac": rate / peak,
+                                 "valu_per_update": sq["SQ_INSTS_VALU"] / r["nnz"],
+                                 "salu_per_update": (sq.get("SQ_INSTS_SALU") or 0) / r["nnz"],
+                                 "note": "instruction counts per launch from the committed rocprofv3 SQ counters "
+                                         "(same kernel sources), rate over this run's average launch"}
     if scheme == "table":
         out["config"]["table_grid"] = r["grid_s"]
     if not args.no_cpu_baseline:

@@ -3,14 +3,16 @@ the epoch kernel on one workload.
 
     python3 bench_profile.py --workload netflix [--scheme hogwild] [bench.py options ...]
 
-runs three passes of bench.py under rocprofv3 (each a child process, each with
+runs four passes of bench.py under rocprofv3 (each a child process, each with
 its own time limit):
 
   1. --kernel-trace --stats: average duration of every kernel;
   2. --pmc FETCH_SIZE and 3. --pmc WRITE_SIZE: bytes the L2 caches read from
-     and write to memory per dispatch (KiB), with a plain 4 GiB device copy
-     in the same run to calibrate both counters (the copy reads and writes
-     exactly 4 GiB, so scale = 4 GiB / counter reading of the copy).
+     and write to the memory fabric per dispatch (KiB), with a plain 4 GiB
+     device copy in the same run to calibrate both counters (the copy reads
+     and writes exactly 4 GiB, so scale = 4 GiB / counter reading of the copy);
+  4. --pmc with six SQ counters: wave instructions issued per dispatch
+     (vector, scalar, vector memory reads and writes), waves and busy cycles.
 
 and writes profiles/<kernel>_<workload>[_<scheme>].md (the summary, with the
 commands) and profiles/traffic_<kernel>_<scheme>_<workload>.json (scaled HBM
@@ -39,6 +41,11 @@ import bench  # noqa: E402  (source_digest, PROFILE_DIR; imports nothing that to
 
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 4 << 30
+SQ_COUNTERS = ("SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_VMEM_WR", "SQ_WAVES",
+               "SQ_BUSY_CYCLES")
+# wave64 vector instructions the chip can issue per second: 256 CUs x 4 SIMDs, each
+# taking 4 cycles (16 lanes) per wave64 instruction, at 2.4 GHz
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 
 
 def say(msg):
@@ -146,15 +153,19 @@ def main():
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         cmds[c] = ["rocprofv3", "--pmc", c, "--output-format", "csv", "-d", os.path.join(out, c), "-o", "run",
                    "--"] + base + ["--steps", "3", "--warmup", "1", "--copy-calibration"]
+    # instruction issue: counts of issued wave instructions per dispatch (8 SQ counters, one pass)
+    cmds["SQ"] = ["rocprofv3", "--pmc", *SQ_COUNTERS, "--output-format", "csv", "-d", os.path.join(out, "SQ"), "-o",
+                  "run", "--"] + base + ["--steps", "2", "--warmup", "1"]
+    passes = ("trace", "FETCH_SIZE", "WRITE_SIZE", "SQ")
     if not a.summarize_only:
-        for key in ("trace", "FETCH_SIZE", "WRITE_SIZE"):
+        for key in passes:
             rc = run_pass(cmds[key], a.limit)
             if rc != 0:
                 # rocprofv3 may end with a segmentation fault after the program has finished;
                 # accept the pass only if its result files are there
                 try:
                     find_csv(os.path.join(out, key), "kernel_stats.csv" if key == "trace" else
-                             "counter_collection.csv")
+                         "counter_collection.csv")
                 except SystemExit:
                     raise SystemExit(f"pass {key} failed with status {rc}")
                 say(f"pass {key}: status {rc} but results are complete; using them")
@@ -187,6 +198,13 @@ def main():
         vals = vals[1:] if len(vals) > 1 else vals
         per_launch[c] = (statistics.median(vals), statistics.median(vals) * 1024.0 * scale[c])
 
+    sq = {}
+    for c in SQ_COUNTERS:
+        disp = counter_per_dispatch(os.path.join(out, "SQ"), c)
+        vals = [v for n, v in disp.values() if short(n).split("<")[0].endswith(kernel)]
+        vals = vals[1:] if len(vals) > 1 else vals
+        sq[c] = statistics.median(vals) if vals else None
+
     w = None
     try:
         from paper_1610_05838_amd import datagen
@@ -207,7 +225,7 @@ def main():
     L = [f"# {kernel} on the {a.workload} workload, {a.scheme} (rocprofv3 summaries)", "",
          "Made by `python3 bench_profile.py --workload " + a.workload + " --scheme " + a.scheme +
          (" -- " + " ".join(extra) if extra else "") + "`, which runs these passes (from /tmp):", ""]
-    for key in ("trace", "FETCH_SIZE", "WRITE_SIZE"):
+    for key in passes:
         L.append("    " + " ".join(x.replace(out, "$OUT").replace(ROOT, "$REPO") for x in cmds[key]))
     L += ["", "$OUT is the directory the raw rocprofv3 output was written to (not committed).",
           "", "## Kernel statistics (kernel trace)", "",
@@ -218,7 +236,9 @@ def main():
                  f"{100 * float(r['TotalDurationNs']) / total:.2f}% |")
     L += ["", f"Epoch kernel `{kernel}`: {len(timed)} timed launches (after the warm-up epoch), average "
               f"{avg_ns / 1e6:.3f} ms, min {min(timed) / 1e6:.3f}, max {max(timed) / 1e6:.3f}.", "",
-          "## HBM traffic (PMC)", "",
+          "## L2-to-fabric traffic (PMC)", "",
+          "FETCH_SIZE and WRITE_SIZE count the bytes the L2 caches read from and write to the memory fabric; "
+          "reads the Infinity Cache serves are included, so these are an upper bound on HBM bytes.", "",
           f"Calibration: `{COPY_KERNEL}` copies 4 GiB -> 4 GiB; scale FETCH_SIZE x{scale['FETCH_SIZE']:.4f}, "
           f"WRITE_SIZE x{scale['WRITE_SIZE']:.4f} (bytes = KiB x 1024 x scale).", "",
           f"| per launch of `{kernel}` | raw KiB (median of timed launches) | scaled bytes | bytes per update |",
@@ -226,12 +246,25 @@ def main():
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         raw, b = per_launch[c]
         L.append(f"| {c} | {raw:.0f} | {b:.4e} | {b / nnz:.1f} |" if nnz else f"| {c} | {raw:.0f} | {b:.4e} | |")
-    L.append(f"| total HBM | | {hbm:.4e} | {hbm / nnz:.1f} |" if nnz else f"| total HBM | | {hbm:.4e} | |")
+    L.append(f"| total L2-to-fabric | | {hbm:.4e} | {hbm / nnz:.1f} |" if nnz else
+             f"| total L2-to-fabric | | {hbm:.4e} | |")
     if nnz:
         L += ["", f"Algorithmic bytes per update: {bpu} (4k*sizeof(feature)+12, k={k}); updates per launch {nnz}.",
               f"Average launch (trace): {avg_ns / 1e6:.3f} ms -> algorithmic {nnz * bpu / avg_ns:.1f} GB/s "
-              f"({100 * nnz * bpu / avg_ns / bench.HBM_PEAK_GBS:.1f}% of 8 TB/s), measured HBM "
+              f"({100 * nnz * bpu / avg_ns / bench.HBM_PEAK_GBS:.1f}% of 8 TB/s), measured L2-to-fabric "
               f"{hbm / avg_ns:.1f} GB/s ({100 * hbm / avg_ns / bench.HBM_PEAK_GBS:.1f}% of 8 TB/s)."]
+    if sq.get("SQ_INSTS_VALU"):
+        L += ["", "## Instruction issue (PMC)", "",
+              f"Wave instructions issued per launch of `{kernel}` (median of timed launches) and per update.  "
+              f"The chip issues at most {VALU_ISSUE_PEAK / 1e9:.1f} G wave64 vector instructions/s "
+              "(256 CUs x 4 SIMDs, 4 cycles each per wave64 instruction, 2.4 GHz).", "",
+              "| counter | per launch | per update |", "|---|---|---|"]
+        for c in SQ_COUNTERS:
+            if sq.get(c) is not None:
+                L.append(f"| {c} | {sq[c]:.4e} | " + (f"{sq[c] / nnz:.2f} |" if nnz else "|"))
+        rate = sq["SQ_INSTS_VALU"] / (avg_ns * 1e-9)
+        L += ["", f"Vector instruction issue: {rate / 1e9:.1f} G/s over the average launch, "
+                  f"{100 * rate / VALU_ISSUE_PEAK:.1f}% of {VALU_ISSUE_PEAK / 1e9:.1f} G/s."]
     with open(md, "w") as f:
         f.write("\n".join(L) + "\n")
     tj = os.path.join(bench.PROFILE_DIR, f"traffic_{kernel}_{a.scheme}_{a.workload}" + (f"_k{kw}" if kw else "") + ".json")
@@ -241,7 +274,8 @@ def main():
                    "hbm_bytes_per_launch": hbm, "fetch_bytes_per_launch": per_launch["FETCH_SIZE"][1],
                    "write_bytes_per_launch": per_launch["WRITE_SIZE"][1],
                    "copy_scale_fetch": scale["FETCH_SIZE"], "copy_scale_write": scale["WRITE_SIZE"],
-                   "avg_launch_ns_trace": avg_ns, "summary": os.path.basename(md)}, f, indent=1)
+                   "avg_launch_ns_trace": avg_ns, "summary": os.path.basename(md),
+                   "sq_per_launch": sq, "valu_issue_peak_per_s": VALU_ISSUE_PEAK}, f, indent=1)
     say(f"wrote {md} and {tj}")
     print("\n".join(L))
 
