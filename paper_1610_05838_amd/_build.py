@@ -7,6 +7,7 @@ go to ``_build/`` beside the sources; the library lands next to this file.
 from __future__ import annotations
 
 import concurrent.futures as cf
+import hashlib
 import os
 import subprocess
 
@@ -27,23 +28,43 @@ CFLAGS = [
 ]
 
 
+def _inputs_digest(src: str) -> str:
+    """Digest of everything an object is built from: the source, every header
+    beside it and the public headers (taken before compiling, so an edit made
+    while the compiler runs leaves the object marked stale)."""
+    h = hashlib.sha256()
+    deps = [os.path.join(CSRC, src)] + sorted(os.path.join(CSRC, x) for x in os.listdir(CSRC) if x.endswith(".hpp"))
+    deps += sorted(os.path.join(INCLUDE, x) for x in os.listdir(INCLUDE))
+    for d in deps:
+        with open(d, "rb") as f:
+            h.update(os.path.basename(d).encode())
+            h.update(f.read())
+    h.update(" ".join(CFLAGS).encode())
+    return h.hexdigest()
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
+    digest = _inputs_digest(src)
     cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+    with open(obj + ".inputs", "w") as f:
+        f.write(digest + "\n")
     return obj
 
 
 def _stale(src: str) -> bool:
-    """Whether the object of `src` is older than the source or any header."""
+    """Whether the object of `src` was built from other inputs than the
+    current ones (or not at all)."""
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    if not os.path.exists(obj):
+    try:
+        with open(obj + ".inputs") as f:
+            built = f.read().strip()
+    except OSError:
         return True
-    deps = [os.path.join(CSRC, src)] + [os.path.join(CSRC, h) for h in os.listdir(CSRC) if h.endswith(".hpp")]
-    deps += [os.path.join(INCLUDE, h) for h in os.listdir(INCLUDE)]
-    return max(os.path.getmtime(d) for d in deps) > os.path.getmtime(obj)
+    return not os.path.exists(obj) or built != _inputs_digest(src)
 
 
 def build(jobs: int = 4, changed_only: bool = False) -> str:
