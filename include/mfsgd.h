@@ -156,10 +156,11 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  as stay resident on the GPU (the automatic form: at most
  *                  min(m, n) / 20, see MFSGD_BATCH_HOGWILD).
  *   "depth"        samples each wavefront keeps in flight: 1, 2, 4 or 8, or
- *                  0 (default) automatically: 1 for the one-XCD
- *                  batch-Hogwild! form (the automatic form always runs 1) (bound by bandwidth, not
- *                  latency, so one in flight runs as fast and halves the
- *                  updates in flight), 2 elsewhere.  A wavefront forwards
+ *                  0 (default) automatically: 1 for the automatic and the
+ *                  one-XCD batch-Hogwild! forms (bound by one XCD's
+ *                  bandwidth or by atomics, not by latency, so one in flight
+ *                  runs as fast and halves the updates in flight), 2
+ *                  elsewhere.  A wavefront forwards
  *                  its own pending updates, so depth never changes the
  *                  serial semantics of one worker; fewer samples in flight
  *                  also means fresher reads of the rows other workers update.
@@ -247,9 +248,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  partitioned (teams of more than one wavefront, k <= 32),
  *                  a wavefront claims two batches of its open block at
  *                  once, one per half, instead of skipping stores (unless
- *                  "skip_stores" is 1).  At k <= 32 a lone worker computes
- *                  the same bits either way; at wider rows its lane sums
- *                  run in another order.
+ *                  "skip_stores" is 1), and the automatic one-XCD form
+ *                  counts such a wavefront as two workers.  At k <= 32 a
+ *                  lone worker computes the same bits either way; at wider
+ *                  rows its lane sums run in another order.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and

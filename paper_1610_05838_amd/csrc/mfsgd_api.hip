@@ -1340,10 +1340,15 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             want = 1;
         else if (hog && g_opt.workers > 0)
             want = std::max<int64_t>(1, g_opt.workers / s);
-        else if (automatic)
+        else if (automatic) {
             // one XCD: the paper's empirical Hogwild! condition caps the
-            // default; the team never exceeds the XCD's resident slots
+            // workers; the team never exceeds the XCD's resident slots.  At
+            // k <= 32 a wavefront runs two batches at once (below), i.e. two
+            // workers, so it takes half as many wavefronts.
             want = hogwild_condition_workers();
+            if (c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1)
+                want = std::max<int64_t>(2, (want + 1) / 2);
+        }
         else if (hog)
             want = 0;
         else
