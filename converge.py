@@ -18,6 +18,12 @@ workers figures).
       side s.  --uniform draws the workload's users and items uniformly
       instead of Zipf-like.
 
+  python converge.py chain [--workload netflix_fp16] [--grid s]
+      Where a pooled wavefront-update epoch goes: per-block claim and
+      completion stamps of one traced epoch, summarised for the column block
+      holding the most samples (whose blocks run one after another) and for
+      the teams.
+
 Learning rates: "config" is the workload's own schedule (lr * decay^t);
 "paper" is the decaying schedule of the evaluation section,
 s_t = alpha / (1 + beta * t^1.5), with the per-dataset alpha, beta and lambda
@@ -222,9 +228,62 @@ def workers(args):
               + " |")
 
 
+def chain(args):
+    """Where a pooled wavefront-update epoch goes: the per-block claim and
+    completion stamps (debug trace, 100 MHz clock) of one epoch after a
+    warm-up epoch, summarised for the column block holding the most samples
+    (its blocks run one after another) and for the teams."""
+    import numpy as np
+
+    r = Runner(args.workload, args.uniform)
+    w, M = r.w, r.M
+    lr_t, lam = lr_schedule(w, "config")
+    s = args.grid or w.get("grid_s", 32)
+    r.setup("wavefront", s)
+    starts = M.debug_plan_starts(s).cpu().numpy()
+    warm = r.epoch_ms("wavefront", lr_t(0), lam)
+    M.set_option("debug", 2)
+    traced = r.epoch_ms("wavefront", lr_t(1), lam)
+    tr = M.debug_trace(5 * s * s).cpu().numpy().view(np.uint32)
+    M.finalize()
+    cols = tr[:s * s].reshape(s, s).astype(np.int64)                # [team, wave] -> column block
+    clk = tr[3 * s * s:5 * s * s].reshape(s, s, 2).astype(np.int64)  # claim, completion (10 ns ticks)
+    cnt = np.diff(starts).reshape(s, s)                              # [row block, column block] -> samples
+    t0 = clk[:, :, 0].min()
+    c0 = ((clk[:, :, 0] - t0) % (1 << 32)) / 100.0                   # microseconds
+    c1 = ((clk[:, :, 1] - t0) % (1 << 32)) / 100.0
+    n = np.array([[cnt[t, cols[t, x]] for x in range(s)] for t in range(s)])
+    colsum = cnt.sum(axis=0)
+    hot = int(np.argmax(colsum))
+    links = sorted((c0[t, x], c1[t, x], t, x, n[t, x]) for t in range(s) for x in range(s) if cols[t, x] == hot)
+    busy = sum(b - a for a, b, *_ in links)
+    gaps = [links[i + 1][0] - links[i][1] for i in range(len(links) - 1)]
+    rates = [c / (b - a) / 1e3 for a, b, _, _, c in links if b > a and c >= 10_000]
+    span = c1.max()
+    print(f"\n{w['name']}, wavefront-update s = {s}: warm-up epoch {warm:.2f} ms, traced epoch {traced:.2f} ms "
+          f"(debug stamps on), stamped span {span / 1e3:.2f} ms\n")
+    print("| measure | value |")
+    print("|---|---|")
+    print(f"| column block with the most samples | {hot}: {int(colsum[hot]):,} samples "
+          f"({colsum[hot] / cnt.sum():.3f} of all, mean column {cnt.sum() / s / cnt.sum():.3f}) |")
+    print(f"| its blocks busy (sum of claim-to-completion) | {busy / 1e3:.2f} ms ({busy / span:.2f} of the span) |")
+    print(f"| hand-over gaps between its blocks | {sum(gaps) / 1e3:.3f} ms (largest {max(gaps):.1f} us) |")
+    if rates:
+        print(f"| its blocks of >= 10,000 samples: updates/s | median {np.median(rates):.3f} x 10^9, "
+              f"min {min(rates):.3f}, max {max(rates):.3f} |")
+    ends = c1.max(axis=1) / 1e3
+    print(f"| teams' last completion | min {ends.min():.2f} ms, median {np.median(ends):.2f}, max {ends.max():.2f} |")
+    print(f"\nBlocks of column block {hot} in wave order (claim and completion in us from the first claim):\n")
+    print("| wave | team | samples | claimed | completed | updates/s (10^9) |")
+    print("|---|---|---|---|---|---|")
+    for a, b, t, x, c in links:
+        rate = f"{c / (b - a) / 1e3:.3f}" if b > a else "-"
+        print(f"| {x} | {t} | {int(c):,} | {a:.1f} | {b:.1f} | {rate} |")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("exp", choices=["curves", "workers"])
+    ap.add_argument("exp", choices=["curves", "workers", "chain"])
     ap.add_argument("--workload", default="netflix_fp16")
     ap.add_argument("--epochs", type=int, default=0, help="curves: epochs (default 20); workers: timed epochs (default 2)")
     ap.add_argument("--lr", choices=["config", "paper"], default="config")
@@ -235,11 +294,14 @@ def main():
                          "space, 1 XCD-partitioned, 3 free-running partition, 4 one XCD")
     ap.add_argument("--counts", default="32,64,128,256,512,1024,2048,4096,8192")
     ap.add_argument("--uniform", action="store_true", help="users and items drawn uniformly (no Zipf skew)")
+    ap.add_argument("--grid", type=int, default=0, help="chain: grid side (default: the workload's)")
     args = ap.parse_args()
     if args.exp == "curves":
         args.epochs = args.epochs or 20
         args.schemes = args.schemes or "hogwild,wavefront:8,wavefront:32"
         curves(args)
+    elif args.exp == "chain":
+        chain(args)
     else:
         args.epochs = args.epochs or 2
         args.schemes = args.schemes or "hogwild,wavefront:32"
