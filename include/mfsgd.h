@@ -237,21 +237,25 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  *                  waves, no tickets), a cross-check of the ticketed kernel
  *                  whose factors it reproduces bit for bit; 0 (default) the
  *                  persistent ticketed kernel.
- *   "half_waves"   two batch-Hogwild! workers per wavefront, one per half
- *                  of its 64 lanes, each lane holding (padded k)/32 values.
+ *   "half_waves"   two workers per wavefront, one per half of its 64
+ *                  lanes, each lane holding (padded k)/32 values.
  *                  1 (default): at k <= 32 (a row of 32 values fills a
- *                  half); 2: in one address space at every width of
- *                  at most 16 bytes per lane (binary32 k <= 128, binary16
- *                  k <= 256); 0: never (at k <= 32 the upper 32 lanes then
- *                  idle).  In one address space "workers" and the default
- *                  worker count are then counted in half-wavefronts;
- *                  partitioned (teams of more than one wavefront, k <= 32),
- *                  a wavefront claims two batches of its open block at
- *                  once, one per half, instead of skipping stores (unless
- *                  "skip_stores" is 1), and the automatic one-XCD form
- *                  counts such a wavefront as two workers.  At k <= 32 a
- *                  lone worker computes the same bits either way; at wider
- *                  rows its lane sums run in another order.
+ *                  half), and for pooled wavefront-update at wider rows of
+ *                  at most 16 bytes per lane when no column block of the
+ *                  plan holds more than twice the mean share of the
+ *                  samples; 2: everywhere at widths of at most 16 bytes per
+ *                  lane (binary32 k <= 128, binary16 k <= 256); 0: never (at
+ *                  k <= 32 the upper 32 lanes then idle).  In one address
+ *                  space "workers" and the default worker count are then
+ *                  counted in half-wavefronts.  Block-scheduled with teams
+ *                  of more than one wavefront, a wavefront claims two
+ *                  batches of its open block at once and runs one per half:
+ *                  at k <= 32 (batch-Hogwild!) instead of skipping stores
+ *                  (unless "skip_stores" is 1), at wider rows with skipped
+ *                  stores where "skip_stores" calls for them; the automatic
+ *                  one-XCD form counts such a wavefront as two workers.  At
+ *                  k <= 32 a lone worker computes the same bits either way;
+ *                  at wider rows its lane sums run in another order.
  *   "table_grid"   grid side of MFSGD_GLOBAL_TABLE, 1 to 1024 (default 256).
  *   "table_workers" MFSGD_GLOBAL_TABLE workers (wavefronts); 0 (default) =
  *                  table_grid / 2 (at least 1): about twice as many row and

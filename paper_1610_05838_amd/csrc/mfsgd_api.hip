@@ -85,6 +85,7 @@ struct Plan {
     int64_t* bstart = nullptr; // kMaxGrid^2 + 1
     std::vector<int64_t> hstart; // host copy of bstart[0 .. s*s]
     double hot_col = 0.0;        // largest share of a column block's samples held by one item
+    double col_peak = 0.0;       // samples of the fullest column block over the mean column block
     double hot_row = 0.0;        // largest share of a row block's samples held by one user
     uint64_t version = 0;        // bumped by every build
     bool matches(const mfsgd_sample* p, int64_t n) const { return src == p && nnz == n && src != nullptr; }
@@ -420,6 +421,10 @@ bool rows_fit_31_bits()
 // wavefront and at most min(m, n) / 20 workers (the paper's empirical
 // Hogwild! condition, section 5.5.1).
 constexpr int kOneXcdShareInv = 64;
+
+// Wavefront-update plans whose fullest column block holds at most this many
+// times the mean run two batches per claim at rows wider than 32 values.
+constexpr double kPairsColumnPeak = 2.0;
 
 bool partitioned_hogwild()
 {
@@ -854,6 +859,16 @@ int build_plan(Plan& pl, const mfsgd_sample* samples, int64_t nnz, int s, bool b
     HIPCHK(hipMemcpyAsync(pl.hstart.data(), pl.bstart, sizeof(int64_t) * pl.hstart.size(), hipMemcpyDeviceToHost,
                           st));
     HIPCHK(hipStreamSynchronize(st));
+    {
+        int64_t top = 0;
+        for (int j = 0; j < s; ++j) {
+            int64_t col = 0;
+            for (int t = 0; t < s; ++t)
+                col += pl.hstart[(size_t)t * s + j + 1] - pl.hstart[(size_t)t * s + j];
+            top = std::max(top, col);
+        }
+        pl.col_peak = nnz > 0 ? (double)top * s / (double)nnz : 0.0;
+    }
     pl.version += 1;
     pl.src = samples;
     pl.nnz = nnz;
@@ -1173,7 +1188,7 @@ int team_layout(const Plan& pl, int64_t want, bool half, EpochLaunch& a)
             CHK(build_team_layout(load, nx, cap / nx, want > 0 ? (want + 3) / 4 : 0, L));
         }
         CHK(grow(&c.tmap, &c.tmap_cap, L.grid, "team map"));
-        CHK(grow(&c.sink, &c.sink_cap, L.grid * waves * 2 * c.KP * (int64_t)elem_size(c.dtype), "store sink"));
+        CHK(grow(&c.sink, &c.sink_cap, L.grid * waves * 4 * c.KP * (int64_t)elem_size(c.dtype), "store sink"));
         if (!c.tsize)
             CHK(dalloc((void**)&c.tsize, sizeof(int32_t) * kMaxGrid, "team sizes"));
         if (!c.xteams)
@@ -1346,7 +1361,8 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             // k <= 32 a wavefront runs two batches at once (below), i.e. two
             // workers, so it takes half as many wavefronts.
             want = hogwild_condition_workers();
-            if (c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1)
+            if ((c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1) ||
+                (g_opt.half_waves == 2 && c.KP > 32 && half_wave_workers(c.KP, c.dtype)))
                 want = std::max<int64_t>(2, (want + 1) / 2);
         }
         else if (hog)
@@ -1357,16 +1373,26 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         a.S = pl->Sp;
         a.bstart = pl->bstart;
         a.s = s;
-        const bool pairs = hog && want != 1 && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1;
+        // Pooled wavefronts that claim two batches at a time and run one per
+        // half: block-scheduled batch-Hogwild! at k <= 32, in place of
+        // skipped stores (measured faster on the Netflix shape at k = 32); at
+        // wider rows, with skipped stores where the plan calls for them, for
+        // both schedules with option half_waves = 2 and, by default, for
+        // wavefront-update on a plan whose column blocks hold at most twice
+        // their mean share (Hugewiki shape: 265 vs 280 ms per epoch; where one
+        // column block bounds the epoch, the coarser claims lengthen its
+        // chain: Netflix shape 21-22 vs 15 ms).  One-wavefront teams keep one
+        // batch per wavefront: their blocks run in order.
+        const bool narrow_pairs = hog && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1;
+        const bool wide_fit = c.KP > 32 && (int64_t)c.KP * (int64_t)elem_size(c.dtype) <= 16 * 32;
+        const bool wide_pairs = wide_fit && (g_opt.half_waves == 2 || (g_opt.half_waves == 1 && !hog &&
+                                                                       pl->col_peak <= kPairsColumnPeak));
+        const bool pairs = want != 1 && (narrow_pairs || wide_pairs);
         CHK(team_layout(*pl, want, pairs, a));
         if (pairs) {
-            // Partitioned batch-Hogwild! at k <= 32: pooled wavefronts claim
-            // two batches at a time and run one per half, in place of skipped
-            // stores (measured faster on the Netflix shape at k = 32; pairs
-            // were slower for wavefront-update, which keeps one batch per
-            // wavefront, as do one-wavefront teams, whose blocks run in order).
             a.half = 1;
-            a.sink = nullptr;
+            if (narrow_pairs)
+                a.sink = nullptr;
         }
         if (atomic) {
             if (a.depth != 1 || a.half || (c.dtype == MFSGD_FP16 && c.KP < 128))

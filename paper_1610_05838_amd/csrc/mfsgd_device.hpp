@@ -801,11 +801,17 @@ __device__ __forceinline__ void run_worker(const Sample* __restrict__ S, int64_t
 // idle lanes add zeros) at KP = 32, so a lone worker computes the same bits
 // either way there; wider rows sum their products in another order.
 // ---------------------------------------------------------------------------
-template <int KP, typename T, int D, bool DBG, bool BUF = false>
+//
+// SKIP (block-scheduled epochs at rows wider than 32 values): as in
+// run_worker, a row that one of the half's next D-1 samples updates again is
+// stored to the half's private sink row instead (sink: 4 rows per wavefront,
+// P and Q of lanes 0-31, then of lanes 32-63).
+template <int KP, typename T, int D, bool DBG, bool BUF = false, bool SKIP = false>
 __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, int64_t nnz, int64_t W, int64_t wave,
                                                 int f, T* __restrict__ P, T* __restrict__ Q, float lr, float lp,
                                                 float lq, const DebugSink dbg,
-                                                const CacheSync sync = CacheSync{0, false, false})
+                                                const CacheSync sync = CacheSync{0, false, false},
+                                                T* __restrict__ sink = nullptr)
 {
     constexpr int H = 32;      // positions per chunk and half; lanes per half
     constexpr int E = KP / H;  // values per lane
@@ -813,6 +819,7 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
     typedef typename VecT<T, E>::type V;
     static_assert(KP % H == 0 && sizeof(V) <= 16, "rows of 32 to 512 values, at most 16 bytes per lane");
     static_assert(!BUF || sizeof(V) == 4, "buffer rows: one dword per lane");
+    static_assert(!(BUF && SKIP), "buffer rows: no store redirection");
     static_assert(H % D == 0 && D <= 16, "depth must divide 32");
 
     const int lane = lane_id();
@@ -942,6 +949,19 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
             if constexpr (BUF) {
                 bp.template st<V>(np, cb + (uint32_t)u * kRowBytes, 0);
                 bq.template st<V>(nq, cb + (uint32_t)v * kRowBytes, 0);
+            } else if constexpr (SKIP) {
+                // the half's next D-1 samples (issued, so processed before
+                // this half stops) take a row they update again from this one
+                // by forwarding
+                bool p_again = false, q_again = false;
+#pragma unroll
+                for (int d = 1; d < D; ++d) {
+                    const int h = (j + d) % D;
+                    p_again |= su[h] == u;
+                    q_again |= sv[h] == v;
+                }
+                R::st(p_again ? sink + (hi ? 2 * KP : 0) + col : P + (int64_t)u * KP + col, np);
+                R::st(q_again ? sink + (hi ? 3 * KP : KP) + col : Q + (int64_t)v * KP + col, nq);
             } else {
                 R::st(P + (int64_t)u * KP + col, np);
                 R::st(Q + (int64_t)v * KP + col, nq);

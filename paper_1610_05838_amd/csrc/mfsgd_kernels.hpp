@@ -122,7 +122,8 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
                                                  DebugSink dbg, int32_t* trace, T* __restrict__ sink,
                                                  Coherence coh)
 {
-    static_assert(!HALF || (KP == 32 && !SKIP), "half-wavefront workers: rows of 32 values, no store redirection");
+    static_assert(!HALF || (KP == 32 ? !SKIP : kHalfRows<KP, T>),
+                  "half-wavefront workers: at most 16 bytes of a row per lane; at 32 values no store redirection");
     constexpr uint32_t kClaim = HALF ? 2u : 1u; // batches per head claim
     constexpr uint32_t kUnit = 64;              // samples per claim unit
     __shared__ int Cperm[kMaxGrid], Ooff[kMaxGrid];
@@ -163,8 +164,9 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
     uint32_t* const stamps = trace ? reinterpret_cast<uint32_t*>(trace) + (int64_t)s * s : nullptr;
     // after the event stamps: the same two moments on the 100 MHz realtime clock (low 32 bits)
     uint32_t* const clocks = trace ? stamps + 2 * (int64_t)s * s : nullptr;
-    // two private rows per wavefront of the grid for skipped stores
-    T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * 2 * KP : nullptr;
+    // private rows per wavefront of the grid for skipped stores: P and Q (of
+    // each half with HALF); the grid's sink holds four per wavefront
+    T* const my_sink = SKIP ? sink + ((int64_t)blockIdx.x * waves + wv) * (HALF ? 4 : 2) * KP : nullptr;
 
     // lane j < nt watches the j-th team of this wavefront's preference order:
     // the home team, then the other teams of the XCD in list order
@@ -299,8 +301,11 @@ __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, 
         blk.trace = nullptr;
         if (blk.orig)
             blk.orig += b0;
-        if constexpr (HALF)
+        if constexpr (HALF && KP == 32)
             run_worker_half<KP, T, D, DBG>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk);
+        else if constexpr (HALF)
+            run_worker_half<KP, T, D, DBG, false, SKIP>(Sp + b0, cnt, 2, 0, f, P, Q, lr, lp, lq, blk,
+                                                        CacheSync{0, false, false}, my_sink);
         else
             run_worker<KP, T, D, DBG, SKIP, false, kCohOff, ATOM>(Sp + b0, cnt, 1, 0, f, P, Q, lr, lp, lq, blk,
                                                                  CacheSync{0, false, false}, my_sink, coh);
@@ -528,6 +533,16 @@ static int occupancy_blocked_t(int threads, bool half)
                                                                 threads, 0) == hipSuccess
                        ? blocks
                        : 0;
+    } else if constexpr (kHalfRows<KP, T>) {
+        if (half) { // both variants such launches may use
+            int skip = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_blocked<KP, T, D, false, false, true>, threads,
+                                                             0) != hipSuccess ||
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&skip, k_blocked<KP, T, D, false, true, true>, threads,
+                                                             0) != hipSuccess)
+                return 0;
+            return blocks < skip ? blocks : skip;
+        }
     }
     // the co-residency cap must hold for both variants the launcher may pick
     int plain = 0;
@@ -696,6 +711,24 @@ static hipError_t launch_epoch_d(const EpochLaunch& a, hipStream_t st)
                                    dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx, a.pool, a.prio,
                                    a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f, a.tickets, a.sched,
                                    a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
+                return hipGetLastError();
+            }
+        }
+        if constexpr (KP > 32 && kHalfRows<KP, T>) {
+            if (a.half) {
+                // two batches per claim at wider rows (option half_waves = 2),
+                // with skipped stores where the plan calls for them (never in
+                // epochs with debug output)
+                if (!DBG && a.sink)
+                    hipLaunchKernelGGL((k_blocked<KP, T, D, false, true, true>), dim3((unsigned)a.grid),
+                                       dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx,
+                                       a.pool, a.prio, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f,
+                                       a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave, (T*)a.sink, acoh);
+                else
+                    hipLaunchKernelGGL((k_blocked<KP, T, D, DBG, false, true>), dim3((unsigned)a.grid),
+                                       dim3(64 * a.wg_waves), 0, st, a.S, a.bstart, a.s, a.xslots, a.tmap, a.xteams, a.nx,
+                                       a.pool, a.prio, a.free_run, a.sigma_c, a.sigma_o, a.tail, P, Q, a.lr, a.lp, a.lq, a.f,
+                                       a.tickets, a.sched, a.spin_limit, a.err, dbg, a.trace_wave, (T*)nullptr, acoh);
                 return hipGetLastError();
             }
         }

@@ -263,6 +263,42 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
     assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf))
 
 
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("scheme,skip", [("hogwild", 0), ("hogwild", 1), ("wavefront", 0), ("wavefront", 1)])
+def test_block_scheduled_wide_pairs_equal_schedule_order(M, dtype, scheme, skip):
+    """Two batches per claim at k = 128 (option half_waves = 2: each lane of
+    a half holds four values of a row), with and without skipped stores, under
+    the partitioned batch-Hogwild! and wavefront-update schedules: on blocks
+    whose concurrently runnable batches commute the result is the oracle's
+    update in the wavefront block order (section 3.2.3) within the usual
+    bounds, and a second run gives the same bits."""
+    rng = np.random.default_rng(77 + skip + (scheme == "wavefront"))
+    s, f = 8, 64
+    G, gu, gv = 6, 3, 2
+    S, m, n = disjoint_block_samples(rng, s, f, G, gu, gv)
+    k, seed = 128, 31
+    opts = dict(batch_f=f, balance=0, partition=1, hogwild_grid=s, skip_stores=skip, half_waves=2)
+    runs = []
+    for rep in range(2):
+        o = dict(DEFAULTS, dtype=1 if dtype == np.float16 else 0, **opts)
+        M.reset_options()
+        for key, val in o.items():
+            M.set_option(key, val)
+        M.init(m, n, k, seed)
+        dS = M.samples_to_device(S)
+        if scheme == "wavefront":
+            M.plan(dS, s)
+        for _ in range(2):
+            M.epoch(dS, 0.01, 0.05, 0.04, scheme)
+        runs.append(tuple(x.cpu().numpy().astype(dtype) for x in M.get_factors(m, n, k)))
+    Po, Qo = oracle.init_factors(m, n, k, seed, dtype)
+    for t in range(2):
+        oracle.epoch_wavefront(Po, Qo, S, 0.01, 0.05, 0.04, s, seed, t, balanced=False)
+    P, Q = runs[0]
+    assert maxabs(P, Po) <= TOL[dtype] and maxabs(Q, Qo) <= TOL[dtype]
+    assert np.array_equal(bits(runs[1][0]), bits(P)) and np.array_equal(bits(runs[1][1]), bits(Q))
+
+
 @pytest.mark.parametrize("half", [1, 0])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
 @pytest.mark.parametrize("s", [8, 16])
