@@ -329,11 +329,14 @@ def measure(args, name, scheme, steps, warmup, dev, host_prefix=0):
     log(f"{name}: test rmse after each epoch: " + ", ".join(f"{x:.4f}" for x in rmses))
     form = mfsgd.get_option("hogwild_form") if scheme == "hogwild" and not args.staged else -1
     atomic = mfsgd.get_option("hogwild_atomic") if form >= 0 else 0
+    pairs = kernel == "k_blocked" and mfsgd.get_option("blocked_pairs") == 1
     r = dict(w=w, scheme=scheme, grid_s=grid_s, nnz=nnz, ntest=len(T), epoch_ms=epoch_ms, rmses=rmses, wall=wall,
              kernel=kernel, S=S, dtype=dtype, resident=mfsgd.get_option("resident_waves"),
              partitioned=scheme == "hogwild" and mfsgd.get_option("partitioned") == 1 and not args.staged,
-             form={-1: "", 0: "one address space", 1: "XCD-partitioned", 3: "XCD-partitioned, free-running",
-                   4: "one XCD"}.get(form, str(form)) + (", atomic adds" if atomic else ""))
+             form=", ".join(x for x in ({-1: "", 0: "one address space", 1: "XCD-partitioned",
+                                         3: "XCD-partitioned, free-running", 4: "one XCD"}.get(form, str(form)),
+                                        "atomic adds" if atomic else "",
+                                        "two batches per claim" if pairs else "") if x))
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)

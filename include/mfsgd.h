@@ -275,7 +275,10 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * batch-Hogwild! epoch, values of "partition" other than 2; -1 before one),
  * "hogwild_atomic" (whether it added its updates atomically),
  * "half_workers" (whether its one-address-space form runs two workers per
- * wavefront for this model),
+ * wavefront for this model), "blocked_pairs" (whether the last
+ * block-scheduled epoch, wavefront-update or block-scheduled
+ * batch-Hogwild!, had each wavefront claim two batches and run one per half;
+ * -1 before one),
  * "table_blocks" (non-empty blocks of the last global-table plan, 0 before one),
  * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
  * block-scheduled kernel), "teams_grid" (workgroups of the last

@@ -157,6 +157,7 @@ struct Context {
     unsigned long long* maxdeg = nullptr; // 2 device words for them
     int last_form = -1;     // form of the last batch-Hogwild! epoch (values of option "partition"), -1 before one
     int last_atomic = 0;    // whether it added its updates atomically
+    int last_pairs = -1;    // whether the last block-scheduled epoch claimed two batches per wavefront, -1 before one
     // planner scratch
     int64_t* counts = nullptr;
     int64_t counts_cap = 0;
@@ -524,7 +525,8 @@ int get_option_impl(const char* key, int64_t* value)
                     !std::strcmp(key, "blocked_per_cu") || !std::strcmp(key, "partitioned") ||
                     !std::strcmp(key, "teams_grid") || !std::strcmp(key, "table_blocks") ||
                     !std::strcmp(key, "half_workers") || !std::strcmp(key, "hogwild_form") ||
-                    !std::strcmp(key, "hogwild_atomic") || !std::strcmp(key, "xcd_round_robin");
+                    !std::strcmp(key, "hogwild_atomic") || !std::strcmp(key, "xcd_round_robin") ||
+                    !std::strcmp(key, "blocked_pairs");
     if (!ro)
         return fail(MFSGD_EINVAL, std::string("unknown option '") + key + "'");
     if (!g.inited)
@@ -545,6 +547,8 @@ int get_option_impl(const char* key, int64_t* value)
         *value = g.last_form;
     else if (!std::strcmp(key, "hogwild_atomic"))
         *value = g.last_atomic;
+    else if (!std::strcmp(key, "blocked_pairs"))
+        *value = g.last_pairs;
     else if (!std::strcmp(key, "teams_grid"))
         *value = g.lay_plan ? g.lay_grid : 0;
     else if (!std::strcmp(key, "table_blocks"))
@@ -599,6 +603,7 @@ int init_impl(int64_t m, int64_t n, int32_t k, uint64_t seed)
     Context& c = g;
     c.last_form = -1;
     c.last_atomic = 0;
+    c.last_pairs = -1;
     c.stats = RowStats();
     HIPCHK(hipGetDevice(&c.device));
     if (c.device >= 0 && c.device < kMaxDevices && !g_rmse_scratch[c.device]) {
@@ -1446,6 +1451,7 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
             else
                 HIPCHK(epoch_f32(a, st));
         }
+        c.last_pairs = a.half ? 1 : 0;
     }
     if (hog) {
         c.last_form = form;

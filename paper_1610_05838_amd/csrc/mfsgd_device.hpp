@@ -878,17 +878,19 @@ __device__ __forceinline__ void run_worker_half(const Sample* __restrict__ S, in
         sp[d] = sq[d] = hp[d] = hq[d] = V{};
     }
 
-    // request the rows of each half's sample at position xl of a chunk
+    // request the rows of each half's sample at position xl of a chunk.  Lane
+    // xl of each half holds it; one backward permute per field hands it to
+    // every lane of that half (the loop bounds are wave-uniform, so all 64
+    // lanes are active here), in place of two lane reads and a select.
+    const int src_half = hi ? 4 * H : 0; // byte address of lane 32
     auto issue = [&](int slot, int mu, int mv, float mr, int xl, int k0, int k1) {
         const bool ok = xl < (hi ? k1 : k0);
-        const int u0 = __builtin_amdgcn_readlane(mu, xl), u1 = __builtin_amdgcn_readlane(mu, xl + H);
-        const int v0 = __builtin_amdgcn_readlane(mv, xl), v1 = __builtin_amdgcn_readlane(mv, xl + H);
-        const int r0 = __builtin_amdgcn_readlane(__float_as_int(mr), xl);
-        const int r1 = __builtin_amdgcn_readlane(__float_as_int(mr), xl + H);
-        const int u = hi ? u1 : u0, v = hi ? v1 : v0;
+        const int src = src_half + 4 * xl;
+        const int u = __builtin_amdgcn_ds_bpermute(src, mu);
+        const int v = __builtin_amdgcn_ds_bpermute(src, mv);
         su[slot] = ok ? u : -1;
         sv[slot] = ok ? v : -1;
-        sr[slot] = __int_as_float(hi ? r1 : r0);
+        sr[slot] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(mr)));
         if constexpr (BUF) {
             sp[slot] = bp.template ld<V>(cb + (uint32_t)(ok ? u : 0) * kRowBytes, 0);
             sq[slot] = bq.template ld<V>(cb + (uint32_t)(ok ? v : 0) * kRowBytes, 0);

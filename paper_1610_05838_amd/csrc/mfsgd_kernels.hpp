@@ -107,9 +107,11 @@ __global__ __launch_bounds__(kHogwildBlock) void k_hogwild_half(const Sample* __
 // the block of wave w+1 must be claimed only after the block of wave w was
 // completed; the host checks that from the stamps.
 //
-// HALF (rows of 32 values, KP = 32): a wavefront claims two consecutive
-// batches of the block at once and runs them as two workers, one per half
-// (run_worker_half); the block's finished count advances by the batches run.
+// HALF (rows of at most 16 bytes per half-wavefront lane): a wavefront claims
+// two consecutive batches of the block at once and runs them as two workers,
+// one per half (run_worker_half); the block's finished count advances by the
+// batches run.  At KP = 32 this replaces skipped stores; at wider rows SKIP
+// applies per half.
 
 template <int KP, typename T, int D, bool DBG, bool SKIP, bool HALF = false, bool ATOM = false>
 __global__ __launch_bounds__(256) void k_blocked(const Sample* __restrict__ Sp, const int64_t* __restrict__ bstart,

@@ -136,6 +136,9 @@ def test_fp16_wavefront_s32_full_size(M, netflix16):
     for t in range(1, 3):
         M.epoch(dS, w["lr"] * w["decay"] ** t, w["lam"], w["lam"], "wavefront")
         hist.append(M.rmse(dT))
+    # the hot item's column block holds four times its share: one batch per
+    # claim, so the blocks of that column get twice as many claimants
+    assert M.get_option("blocked_pairs") == 0
     say(f"netflix fp16 wavefront s={s} test rmse {hist}")
     # The block order need not lower the test RMSE every epoch here: one item
     # holds 9.6% of the ratings (Zipf 1.0 over 17,770 items), so each epoch
@@ -285,6 +288,9 @@ def test_hugewiki_full_size_wavefront_s64(M, gen, hugewiki):
     M.set_option("debug", 0)
     hist.append(M.rmse(dT))
     M.epoch(dS, w["lr"], w["lam"], w["lam"], "wavefront")
+    # uniform items: no column block holds more than twice its share, so each
+    # wavefront claims two batches and runs one per half
+    assert M.get_option("blocked_pairs") == 1
     hist.append(M.rmse(dT))
     say(f"hugewiki wavefront s={s} test rmse {hist}")
     assert all(b < a for a, b in zip(hist, hist[1:]))

@@ -423,6 +423,44 @@ def test_wide_rows_schedule_and_coverage(M, dtype):
         assert np.array_equal(M.debug_trace(nb).cpu().numpy(), oracle.hogwild_batch_owner(nnz, f, Wd))
 
 
+def test_blocked_pairs_choice(M):
+    """Read-only key blocked_pairs: -1 before a block-scheduled epoch (a
+    one-address-space epoch leaves it there).  Pooled wavefront-update at
+    k = 128 claims two batches per wavefront when no column block of the plan
+    holds more than twice its mean share (uniform items) and one where a hot
+    item's column block does; half_waves = 0 turns it off and 2 on; teams of
+    one wavefront (the deterministic scheme) keep one batch; block-scheduled
+    batch-Hogwild! pairs its claims at k = 32."""
+    rng = np.random.default_rng(5)
+    m, n, nnz, s = 3000, 2000, 200_000, 8
+    uni = np.zeros(nnz, dtype=oracle.SAMPLE_DTYPE)
+    uni["u"] = rng.integers(0, m, nnz)
+    uni["v"] = rng.integers(0, n, nnz)
+    uni["r"] = rng.standard_normal(nnz)
+    hot = uni.copy()
+    hot["v"][::2] = 7  # one item with half of the samples: its column block holds four times its share
+
+    def last(S, k, scheme, **opts):
+        M.reset_options()
+        for key, val in dict(DEFAULTS, **opts).items():
+            M.set_option(key, val)
+        M.init(m, n, k, 3)
+        assert M.get_option("blocked_pairs") == -1
+        dS = M.samples_to_device(S)
+        if scheme != "hogwild":
+            M.plan(dS, s)
+        M.epoch(dS, 0.01, 0.05, 0.04, scheme)
+        return M.get_option("blocked_pairs")
+
+    assert last(uni, 128, "wavefront") == 1
+    assert last(hot, 128, "wavefront") == 0
+    assert last(uni, 128, "wavefront", half_waves=0) == 0
+    assert last(hot, 128, "wavefront", half_waves=2) == 1
+    assert last(uni, 128, "wavefront_det") == 0
+    assert last(uni, 32, "hogwild", partition=1, hogwild_grid=8) == 1
+    assert last(uni, 128, "hogwild") == -1
+
+
 def test_half_workers_choice(M):
     """Read-only key half_workers: two workers per wavefront at k <= 32 by
     default; at every width of at most 16 bytes per lane with half_waves = 2;
