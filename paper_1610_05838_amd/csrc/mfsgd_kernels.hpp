@@ -898,12 +898,14 @@ struct Dispatch {
     }
     static int occupancy_blocked(int KP, int depth, int threads, bool half)
     {
+        // half: two batches per claim, at every width whose half-wavefront
+        // rows fit (the variant holds twice the values per lane)
         switch (KP) {
         case 32: return occupancy_blocked_kp<32, T>(depth, threads, half);
-        case 64: return occupancy_blocked_kp<64, T>(depth, threads, false);
-        case 128: return occupancy_blocked_kp<128, T>(depth, threads, false);
-        case 256: return occupancy_blocked_kp<256, T>(depth, threads, false);
-        case 512: return occupancy_blocked_kp<512, T>(depth, threads, false);
+        case 64: return occupancy_blocked_kp<64, T>(depth, threads, half);
+        case 128: return occupancy_blocked_kp<128, T>(depth, threads, half);
+        case 256: return occupancy_blocked_kp<256, T>(depth, threads, half);
+        case 512: return occupancy_blocked_kp<512, T>(depth, threads, half);
         default: return 0;
         }
     }
