@@ -1384,10 +1384,11 @@ int epoch_impl(const mfsgd_sample* samples, int64_t nnz, float lr, float lp, flo
         // wider rows, with skipped stores where the plan calls for them, for
         // both schedules with option half_waves = 2 and, by default, for
         // wavefront-update on a plan whose column blocks hold at most twice
-        // their mean share (Hugewiki shape: 265 vs 280 ms per epoch; where one
-        // column block bounds the epoch, the coarser claims lengthen its
-        // chain: Netflix shape 21-22 vs 15 ms).  One-wavefront teams keep one
-        // batch per wavefront: their blocks run in order.
+        // their mean share (on the Hugewiki shape about 8 % shorter epochs;
+        // where one column block bounds the epoch, the coarser claims
+        // lengthen its chain, on the Netflix shape about 10 % longer ones).
+        // One-wavefront teams keep one batch per wavefront: their blocks run
+        // in order.
         const bool narrow_pairs = hog && c.KP == 32 && half_wave_workers(c.KP, c.dtype) && g_opt.skip_stores != 1;
         const bool wide_fit = c.KP > 32 && (int64_t)c.KP * (int64_t)elem_size(c.dtype) <= 16 * 32;
         const bool wide_pairs = wide_fit && (g_opt.half_waves == 2 || (g_opt.half_waves == 1 && !hog &&
