@@ -281,8 +281,9 @@ enum { MFSGD_FP32 = 0, MFSGD_FP16 = 1 };
  * -1 before one),
  * "table_blocks" (non-empty blocks of the last global-table plan, 0 before one),
  * "blocked_per_cu" (workgroups per CU the occupancy query reports for the
- * block-scheduled kernel), "teams_grid" (workgroups of the last
- * block-scheduled epoch, 0 before one).
+ * block-scheduled kernel with one batch per claim; the two-batch variant
+ * holds twice the values per lane and may fit fewer), "teams_grid"
+ * (workgroups of the last block-scheduled epoch, 0 before one).
  * Returns MFSGD_EINVAL for an unknown key or an out-of-range value. */
 int mfsgd_set_option(const char* key, int64_t value);
 int mfsgd_get_option(const char* key, int64_t* value);
