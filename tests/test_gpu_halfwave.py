@@ -263,20 +263,21 @@ def test_block_scheduled_pairs_equal_schedule_order(M, dtype, s, skip):
     assert np.array_equal(bits(Ph), bits(Pf)) and np.array_equal(bits(Qh), bits(Qf))
 
 
-@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("dtype,k", [(np.float32, 64), (np.float32, 128), (np.float16, 128), (np.float16, 256)])
 @pytest.mark.parametrize("scheme,skip", [("hogwild", 0), ("hogwild", 1), ("wavefront", 0), ("wavefront", 1)])
-def test_block_scheduled_wide_pairs_equal_schedule_order(M, dtype, scheme, skip):
-    """Two batches per claim at k = 128 (option half_waves = 2: each lane of
-    a half holds four values of a row), with and without skipped stores, under
-    the partitioned batch-Hogwild! and wavefront-update schedules: on blocks
-    whose concurrently runnable batches commute the result is the oracle's
-    update in the wavefront block order (section 3.2.3) within the usual
-    bounds, and a second run gives the same bits."""
+def test_block_scheduled_wide_pairs_equal_schedule_order(M, dtype, k, scheme, skip):
+    """Two batches per claim at rows wider than 32 values (option
+    half_waves = 2: each lane of a half holds k/32 values, 8 to 16 bytes),
+    with and without skipped stores, under the partitioned batch-Hogwild! and
+    wavefront-update schedules: on blocks whose concurrently runnable batches
+    commute the result is the oracle's update in the wavefront block order
+    (section 3.2.3) within the usual bounds, and a second run gives the same
+    bits."""
     rng = np.random.default_rng(77 + skip + (scheme == "wavefront"))
     s, f = 8, 64
     G, gu, gv = 6, 3, 2
     S, m, n = disjoint_block_samples(rng, s, f, G, gu, gv)
-    k, seed = 128, 31
+    seed = 31
     opts = dict(batch_f=f, balance=0, partition=1, hogwild_grid=s, skip_stores=skip, half_waves=2)
     runs = []
     for rep in range(2):
