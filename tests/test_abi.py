@@ -68,3 +68,27 @@ def test_options_without_gpu(libpath):
     assert lib.mfsgd_get_option(b"table_blocks", ctypes.byref(v)) == -4  # read-only, needs init
     lib.mfsgd_get_epoch.restype = ctypes.c_int64
     assert lib.mfsgd_get_epoch() == -1  # not initialised
+
+
+def test_read_only_keys_without_gpu(libpath):
+    """Every read-only key the header lists is known to the library: before
+    mfsgd_init reading one is a state error (not an unknown key), and none can
+    be set."""
+    src = open(HEADER).read()
+    block = src[src.index("Read-only keys"):src.index("int mfsgd_set_option")]
+    keys = sorted(set(re.findall(r'"([a-z_0-9]+)"', block)))
+    assert {"resident_waves", "xcds", "blocked_pairs", "half_workers", "teams_grid"} <= set(keys)
+    lib = ctypes.CDLL(libpath)
+    lib.mfsgd_set_option.argtypes = [ctypes.c_char_p, ctypes.c_int64]
+    lib.mfsgd_get_option.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64)]
+    v = ctypes.c_int64()
+    read_only = []
+    for k in keys:
+        rc = lib.mfsgd_get_option(k.encode(), ctypes.byref(v))
+        if rc == 0:  # a settable option that the text mentions
+            continue
+        assert rc == -4, k                                   # MFSGD_ESTATE, not MFSGD_EINVAL
+        assert lib.mfsgd_set_option(k.encode(), 1) == -1, k  # MFSGD_EINVAL
+        read_only.append(k)
+    assert {"resident_waves", "xcds", "xcd_round_robin", "cus", "partitioned", "hogwild_form", "hogwild_atomic",
+            "half_workers", "blocked_pairs", "table_blocks", "blocked_per_cu", "teams_grid"} <= set(read_only)
